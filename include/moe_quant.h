@@ -1,0 +1,294 @@
+/*
+ * moe_quant.h -- C ABI of the MI355X (gfx950) mixed-precision MoE expert-FFN
+ * kernel library.
+ *
+ * The library implements the inference hot path of DynaMo ("Runtime Switchable
+ * Quantization for MoE with Cross-Dataset Adaptation", arXiv 2503.21135):
+ *   - top-k expert selection (Sec. II-A, "MoE Model"),
+ *   - expert-level mixed-precision uniform quantization with codes packed into
+ *     32-bit words (Sec. IV-A, last paragraph; Sec. V-B "Quantized Weight
+ *     Packing Load"),
+ *   - the channel-level switch that replaces channels of a quantized expert by
+ *     cached higher-precision copies located through (expert, channel) index
+ *     headers (Sec. IV-B "Channel Weights Replacement based on Caching";
+ *     Sec. V-A "Data Format in the Channel Cache"),
+ *   - dequantization fused with the matrix-core contraction (Sec. V-B
+ *     "Channel-Grained Dequantization"), applied to the routed expert FFN.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *   - Every buffer is owned by the caller.  "device" pointers are HIP device
+ *     memory, "host" pointers are ordinary host memory read only during the
+ *     call.  The library keeps no state between calls and allocates nothing.
+ *   - All device work is enqueued on `stream` (a hipStream_t, passed as void*;
+ *     NULL is the default stream) and is asynchronous to the host.  No entry
+ *     point reads device memory back to the host.
+ *   - Arguments are validated on the host before any device work is enqueued;
+ *     a call that returns an error has had no effect.  A HIP launch failure is
+ *     reported as MOE_ERR_HIP; the stream's state is then undefined.
+ *   - bf16 values are passed as uint16_t bit patterns, fp16 values likewise.
+ *   - Setting the environment variable MOE_DEBUG=1 makes every entry point
+ *     synchronise its stream after each launch and check for errors.
+ *
+ * Packed code layout (the contract between moe_quant_pack and the FFN)
+ * ---------------------------------------------------------------------
+ * A row of K codes of bit-width b is stored as K*b/32 little-endian uint32
+ * words.  For b in {2, 4, 8} each word holds 32/b consecutive codes; the
+ * codes of even local index 2i sit at bits [b*i, b*i+b) and the codes of odd
+ * local index 2i+1 at bits [16+b*i, 16+b*i+b) ("half-split" order: the low
+ * half-word holds the even codes, the high half-word the odd ones, each least
+ * significant field first).  For b = 3 every block of 32 codes takes three
+ * words: word 0 holds bits 0..1 of codes 0..15 and word 1 bits 0..1 of codes
+ * 16..31, both in the 2-bit half-split order; word 2 holds bit 2 of codes
+ * 0..31 in the 1-bit half-split order (code 2i at bit i, code 2i+1 at bit
+ * 16+i).  Quantization groups run along K: group j covers codes
+ * [j*group, (j+1)*group) of a row.
+ *
+ * Quantizer (per row and group; Sec. IV-A, uniform quantization)
+ * ----------------------------------------------------------------
+ *   mn = min(0, min w), mx = max(0, max w), qmax = 2^b - 1,
+ *   s  = (mx - mn) / qmax in IEEE binary64,
+ *   s16 = the smallest fp16 value >= s (1.0 when s == 0),
+ *   z  = rint(-mn / s16)            (ties to even, an integer in [0, qmax]),
+ *   q  = clamp(rint(w / s16) + z, 0, qmax),
+ *   dequantized weight = s16 * (q - z)   (exact in fp32).
+ * {s16, z} are stored as one uint32: bits 0..15 the fp16 scale, bits 16..31
+ * the fp16 zero point.
+ *
+ * FFN numerics
+ * ------------
+ * The dequantized weights enter the contraction exactly: the matrix cores
+ * multiply the integer codes (exact in bf16) by bf16 activations with fp32
+ * accumulation, and each group's scale and zero point are applied to the fp32
+ * partial sum.  The only rounding point besides fp32 accumulation is the
+ * hidden activation h = silu(g) * u, which is rounded to bf16 (round to
+ * nearest even) before the down projection, as the paper feeds 16-bit
+ * activations to the matrix cores (Sec. V-B).
+ */
+#ifndef MOE_QUANT_H
+#define MOE_QUANT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define MOE_OK             0
+#define MOE_ERR_ARG       -1  /* bad size, NULL pointer or inconsistent arguments      */
+#define MOE_ERR_BITS      -2  /* bit-width outside {2, 3, 4, 8}                         */
+#define MOE_ERR_ALIGN     -3  /* a pointer that must be 16-byte aligned is not          */
+#define MOE_ERR_WORKSPACE -4  /* workspace NULL or smaller than the size helper returns */
+#define MOE_ERR_SLOT      -5  /* switch slot out of range, duplicated, or two slots
+                                 naming the same (expert, row)                          */
+#define MOE_ERR_RANGE     -6  /* an fp16 scale would overflow (reported by the device
+                                 status word of moe_quant_pack)                         */
+#define MOE_ERR_HIP       -7  /* a HIP call or kernel launch failed                    */
+
+/* Limits checked by the host validation. */
+#define MOE_MAX_EXPERTS  512  /* routed + shared experts of one layer */
+#define MOE_MAX_TOPK      16
+
+/* Kinds of expert weight matrix. */
+#define MOE_KIND_GATE 0   /* [d_ff][d_model]  rows = hidden neurons, K = d_model */
+#define MOE_KIND_UP   1   /* [d_ff][d_model]                                     */
+#define MOE_KIND_DOWN 2   /* [d_model][d_ff]  rows = output channels, K = d_ff   */
+
+/*
+ * One kind (gate, up or down) of every expert of a layer.
+ *
+ * Base codes: expert e (routed experts 0..E-1 first, then shared experts
+ * E..E+S-1) stores its R_e x K_e matrix row-major in the packed layout above
+ * at word offset code_off[e] of `codes` (row stride K_e*bits[e]/32 words).
+ * code_off[e] must be a multiple of 4 (16-byte aligned rows start).
+ * Its scales and zeros are group-major: the {s16, z} word of (row r, group j)
+ * is sz[sz_off[e] + j*R_e + r].
+ *
+ * Resident 8-bit copies (the channel cache of Sec. IV-B / V-A, kept here as
+ * 8-bit codes quantized from the original fp32 rows): slot s holds one row of
+ * a routed expert, K/4 words at copy_codes[s*(K/4)], its {s16, z} words at
+ * copy_sz[s*(K/group) + j], and its header (expert, row) at copy_hdr[2s],
+ * copy_hdr[2s+1].  A layer may have n_slots = 0 (copy pointers then NULL).
+ *
+ * Switch state, written only by moe_set_channel_switch: row_slot[e*R + r] is
+ * the copy slot that row r of routed expert e currently reads, or -1 for its
+ * base codes.
+ */
+typedef struct moe_kind_desc {
+  const uint32_t* codes;          /* device */
+  const uint32_t* sz;             /* device */
+  const int64_t*  code_off;       /* device [E+S] */
+  const int64_t*  sz_off;         /* device [E+S] */
+  const int64_t*  code_off_host;  /* host   [E+S] (validation) */
+  int32_t         n_slots;
+  int32_t         reserved0;
+  const uint32_t* copy_codes;     /* device [n_slots][K/4]      */
+  const uint32_t* copy_sz;        /* device [n_slots][K/group]  */
+  const int32_t*  copy_hdr;       /* device [n_slots][2]        */
+  const int32_t*  copy_hdr_host;  /* host   [n_slots][2]        */
+  int32_t*        row_slot;       /* device [E][R]              */
+} moe_kind_desc_t;
+
+/*
+ * One MoE layer.  Routed experts have hidden size d_ff, shared experts
+ * d_ff_shared (shared experts are always applied with weight 1 and are never
+ * switched).  bits[e] in {2, 3, 4, 8}; bit-width 3 needs group == 128.
+ *
+ * order_gu[e*d_ff + i] and order_dn[e*d_model + i] (routed experts only) are
+ * the orders in which the FFN visits hidden neurons and output channels.  They
+ * are rebuilt by moe_set_channel_switch so that neurons (channels) with the
+ * same precision sources are adjacent; any permutation gives the same result.
+ */
+typedef struct moe_layer {
+  int32_t n_experts;     /* E, routed  */
+  int32_t n_shared;      /* S          */
+  int32_t d_model;
+  int32_t d_ff;
+  int32_t d_ff_shared;
+  int32_t group;         /* 64 or 128  */
+  const int32_t* bits_host;   /* host   [E+S] */
+  const int32_t* bits;        /* device [E+S] */
+  moe_kind_desc_t kind[3];
+  int32_t* order_gu;          /* device [E][d_ff]    */
+  int32_t* order_dn;          /* device [E][d_model] */
+  int32_t* staging;           /* device scratch of at least max(kind[].n_slots)+1 int32 */
+} moe_layer_t;
+
+/*
+ * moe_quant_pack -- quantize rows of an fp32 matrix and pack the codes.
+ * Sec. IV-A (uniform quantization of each expert at its precision) and
+ * Sec. V-B (several low-bit codes packed into one 32-bit word).
+ *
+ *   w        device fp32 [R][ld_w]; the rows to quantize are rows[0..n-1]
+ *            (device int32 list) or, when rows == NULL, rows 0..n-1 (n <= R).
+ *   K        codes per row; K % group == 0, K % 32 == 0.
+ *   bits     2, 3, 4 or 8.     group   64 or 128 (3-bit needs 128).
+ *   codes    device; list row i is written to codes[i*ld_codes ...], K*bits/32
+ *            words; ld_codes >= K*bits/32; codes and ld_codes*4 16-byte aligned.
+ *   sz       device; {s16, z} word of (list row i, group j) is written to
+ *            sz[i*sz_row_stride + j*sz_group_stride].
+ *   status   device int32 or NULL; set to MOE_ERR_RANGE by any group whose
+ *            scale overflows fp16 (that group's scale is then +inf).  Never
+ *            cleared by the library.
+ */
+int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K,
+                   int32_t bits, int32_t group,
+                   const int32_t* rows, int32_t n,
+                   uint32_t* codes, int64_t ld_codes,
+                   uint32_t* sz, int64_t sz_row_stride, int64_t sz_group_stride,
+                   int32_t* status, void* stream);
+
+/*
+ * moe_route_permute -- router, top-k selection and token permutation.
+ * Sec. II-A (a fixed number K of experts selected per token); the paper's
+ * one-to-many mapping of a token to the channels of several experts
+ * (Sec. I, Sec. II-A "Data-Weight Mappings") becomes per-expert segments.
+ *
+ *   x         device bf16 [T][d]
+ *   w_router  device fp32 [E][d];  bias  device fp32 [E] or NULL
+ *   logit[t][e] = (sum_c x[t][c]*w_router[e][c]) + bias[e], computed in fp32
+ *             in this fixed order: 64 partial sums, partial l accumulating
+ *             fmaf over c = l, l+64, l+128, ... in increasing c; then for
+ *             off = 32, 16, 8, 4, 2, 1: partial[l] += partial[l+off] (l < off).
+ *   topk_ids  device int32 [T][k]: the k experts of largest logit, ordered by
+ *             (logit descending, expert index ascending).
+ *   topk_w    device fp32 [T][k]: softmax over the k selected logits,
+ *             m = logit of slot 0, e_j = cexp(l_j - m), S = e_0 + e_1 + ...
+ *             summed left to right, w_j = e_j / S.  cexp is the library's
+ *             exponential for arguments <= 0: 0 below -80, otherwise
+ *             n = rint(x*fl(log2 e)), r = x - n*ln2 by a two-constant
+ *             Cody-Waite reduction with fmaf (ln2 split into its leading 12
+ *             significant bits and the fp32 remainder), the degree-7 Taylor
+ *             polynomial of e^r with fp32 coefficients 1/i! by Horner fmaf,
+ *             scaled by 2^n.
+ *   offsets   device int32 [E+S+1]: segment e (routed) holds the rows of the
+ *             tokens that selected e, tokens in increasing order; segment E+s
+ *             (shared expert s) holds all T tokens in order.  offsets[0] = 0.
+ *   perm_token device int32 [T*(k+S)]: token of each permuted row.
+ *   inv_perm  device int32 [T][k+S]: row of (t, topk slot j) for j < k, and of
+ *             (t, shared expert s) at j = k+s.
+ *   x_perm    device bf16 [T*(k+S)][d] or NULL: x[perm_token[p]] (bit copy).
+ *   ws        device workspace of at least moe_route_workspace_bytes(T,E,k,S).
+ *   Requires d % 64 == 0, 1 <= k <= min(E, MOE_MAX_TOPK), E+S <= MOE_MAX_EXPERTS.
+ *   Results are bitwise reproducible.
+ */
+int moe_route_permute(const uint16_t* x, int32_t T, int32_t d,
+                      const float* w_router, const float* bias,
+                      int32_t E, int32_t k, int32_t S,
+                      int32_t* topk_ids, float* topk_w,
+                      int32_t* offsets, int32_t* perm_token, int32_t* inv_perm,
+                      uint16_t* x_perm,
+                      void* ws, size_t ws_bytes, void* stream);
+
+size_t moe_route_workspace_bytes(int32_t T, int32_t E, int32_t k, int32_t S);
+
+/*
+ * moe_ffn_plan -- the output split count and workspace size of
+ * moe_expert_ffn_mixed for this layer and batch.  Depends only on host-known
+ * shapes.  Either output pointer may be NULL.
+ */
+int moe_ffn_plan(const moe_layer_t* L, int32_t T, int32_t k,
+                 int32_t* n_split, size_t* ws_bytes);
+
+/*
+ * moe_expert_ffn_mixed -- the routed (and shared) expert FFNs of one layer
+ * over per-expert mixed-precision packed weights, with the channel switch
+ * applied row by row.  Sec. IV-A (expert-level precisions), Sec. IV-B and
+ * V-A (switched channels read their cached copy), Sec. V-B (packed loads,
+ * on-chip unpacking, dequantization fused into the matrix-core contraction).
+ *
+ * For permuted row p of segment e (token t = perm_token[p]):
+ *   g = Wg_e x_t,  u = Wu_e x_t,  h = bf16(silu(g) * u),  o_p = Wd_e h
+ * where each row of W*_e is the dequantized copy slot row_slot[e][row] when
+ * that is >= 0 and the dequantized base codes otherwise.
+ *
+ *   x          device bf16 [T][d_model], original token order.
+ *   offsets, perm_token   from moe_route_permute (T*k routed rows, S*T shared).
+ *   o          device fp32 [n_split][T*(k+S)][d_model]; the FFN output of row p
+ *              is the sum over the n_split slices (moe_ffn_plan), which
+ *              moe_unpermute_combine adds.  16-byte aligned.
+ *   ws         device workspace of at least moe_ffn_plan()'s ws_bytes.
+ *   Never reads offsets on the host: the grid covers the worst case and idle
+ *   waves exit.
+ */
+int moe_expert_ffn_mixed(const moe_layer_t* L, const uint16_t* x, int32_t T,
+                         int32_t k, const int32_t* offsets,
+                         const int32_t* perm_token, float* o,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * moe_set_channel_switch -- install a set of cached 8-bit copies.
+ * Sec. IV-B "Channel Weights Replacement based on Caching" and Sec. V-A "Data
+ * Format in the Channel Cache": the copy of each listed slot replaces the row
+ * named by its (expert, row) header; every other row of that kind reverts to
+ * its base codes.  No requantization takes place.
+ *
+ *   kind      MOE_KIND_GATE/UP/DOWN, or -1 with n_on == 0 to reset all kinds.
+ *   slots_on  host int32 list of n_on distinct slots in [0, n_slots) whose
+ *             headers name distinct rows; copied before the call returns.
+ *   Rewrites kind[kind].row_slot and order_gu (gate/up) or order_dn (down).
+ */
+int moe_set_channel_switch(moe_layer_t* L, int32_t kind,
+                           const int32_t* slots_on, int32_t n_on, void* stream);
+
+/*
+ * moe_unpermute_combine -- y[t] = sum_j topk_w[t][j] * o[inv_perm[t][j]]
+ *                                + sum_s o[inv_perm[t][k+s]],
+ * where o[p] = sum over the n_split slices at o + i*split_stride.  fp32.
+ *   y device fp32 [T][d]; o, y 16-byte aligned, d % 4 == 0.
+ */
+int moe_unpermute_combine(const float* o, int32_t n_split, int64_t split_stride,
+                          const int32_t* inv_perm, const float* topk_w,
+                          int32_t T, int32_t k, int32_t S, int32_t d,
+                          float* y, void* stream);
+
+/* Human-readable name of a status code. */
+const char* moe_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_QUANT_H */

@@ -1,0 +1,289 @@
+"""CPU oracle of the mixed-precision MoE expert-FFN hot path (DynaMo,
+arXiv 2503.21135).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py``; the product path never imports it.
+It shares no code with the GPU library: ``oracle.c`` is compiled by gcc alone
+and this module only marshals numpy arrays into it.
+
+The arithmetic lives in ``oracle.c``; ``layer_forward`` below strings its
+steps together in the paper's order: route (Sec. II-A), quantize each expert at
+its precision (Sec. IV-A), replace switched rows by their cached copies
+(Sec. IV-B, Sec. V-A), expert FFN, combine.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+OK, ERR_ARG, ERR_BITS, ERR_SLOT, ERR_RANGE = 0, -1, -2, -5, -6
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc (no HIP) into oracle/liboracle.so."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+               "-fno-fast-math", "-fopenmp", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        L = C.CDLL(_LIB_PATH)
+        vp, i32, i64 = C.c_void_p, C.c_int, C.c_int64
+        sig = {
+            "oracle_fp16_value": (C.c_double, [C.c_uint16]),
+            "oracle_fp16_round_up": (C.c_uint16, [C.c_double]),
+            "oracle_bf16_value": (C.c_double, [C.c_uint16]),
+            "oracle_bf16_round": (C.c_uint16, [C.c_double]),
+            "oracle_quantize": (i32, [vp, i64, i32, i32, i32, i32, vp, vp, vp]),
+            "oracle_dequant": (None, [vp, vp, vp, i32, i32, i32, vp]),
+            "oracle_pack": (i32, [vp, i32, i32, i32, vp]),
+            "oracle_unpack": (i32, [vp, i32, i32, i32, vp]),
+            "oracle_cexp": (C.c_float, [C.c_float]),
+            "oracle_route": (i32, [vp, i32, i32, vp, vp, i32, i32, vp, vp, vp]),
+            "oracle_permute": (i32, [vp, i32, i32, i32, i32, vp, vp, vp]),
+            "oracle_switch": (i32, [vp, i32, i32, i32, vp, i32, vp]),
+            "oracle_expert_ffn": (None, [vp, vp, vp, i32, i32, vp, vp, i32, i32, vp]),
+            "oracle_combine": (None, [vp, vp, vp, i32, i32, i32, i32, vp]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+# ---------------------------------------------------------------------------
+# scalar helpers
+# ---------------------------------------------------------------------------
+def fp16_value(h: int) -> float:
+    return lib().oracle_fp16_value(h)
+
+
+def fp16_round_up(s: float) -> int:
+    return lib().oracle_fp16_round_up(s)
+
+
+def bf16_round(v: float) -> int:
+    return lib().oracle_bf16_round(v)
+
+
+def cexp(x: float) -> float:
+    return lib().oracle_cexp(x)
+
+
+def cexp_many(x: np.ndarray) -> np.ndarray:
+    f = lib().oracle_cexp
+    return np.array([f(float(v)) for v in np.asarray(x, np.float32).ravel()],
+                    dtype=np.float32).reshape(np.shape(x))
+
+
+# ---------------------------------------------------------------------------
+# quantization and packing
+# ---------------------------------------------------------------------------
+def quantize(w: np.ndarray, bits: int, group: int):
+    """Returns (status, q uint8 [R][K], s16 uint16 [R][K/g], z16 uint16 [R][K/g])."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    R, K = w.shape
+    q = np.empty((R, K), np.uint8)
+    G = K // group if group > 0 else 0
+    s16 = np.empty((R, max(G, 1)), np.uint16)
+    z16 = np.empty((R, max(G, 1)), np.uint16)
+    st = lib().oracle_quantize(_ptr(w), K, R, K, bits, group, _ptr(q), _ptr(s16), _ptr(z16))
+    return st, q, s16[:, :G], z16[:, :G]
+
+
+def dequant(q: np.ndarray, s16: np.ndarray, z16: np.ndarray, group: int) -> np.ndarray:
+    q = np.ascontiguousarray(q, np.uint8)
+    R, K = q.shape
+    out = np.empty((R, K), np.float64)
+    lib().oracle_dequant(_ptr(q), _ptr(np.ascontiguousarray(s16)),
+                         _ptr(np.ascontiguousarray(z16)), R, K, group, _ptr(out))
+    return out
+
+
+def pack(q: np.ndarray, bits: int) -> np.ndarray:
+    q = np.ascontiguousarray(q, np.uint8)
+    R, K = q.shape
+    out = np.empty((R, K * bits // 32), np.uint32)
+    st = lib().oracle_pack(_ptr(q), R, K, bits, _ptr(out))
+    if st != OK:
+        raise ValueError("oracle_pack: status %d" % st)
+    return out
+
+
+def unpack(words: np.ndarray, K: int, bits: int) -> np.ndarray:
+    words = np.ascontiguousarray(words, np.uint32)
+    R = words.shape[0]
+    out = np.empty((R, K), np.uint8)
+    st = lib().oracle_unpack(_ptr(words), R, K, bits, _ptr(out))
+    if st != OK:
+        raise ValueError("oracle_unpack: status %d" % st)
+    return out
+
+
+def sz_words(s16: np.ndarray, z16: np.ndarray) -> np.ndarray:
+    """{s16, z} per (row, group) as the 32-bit word the library stores."""
+    return s16.astype(np.uint32) | (z16.astype(np.uint32) << 16)
+
+
+# ---------------------------------------------------------------------------
+# routing
+# ---------------------------------------------------------------------------
+def route(x_bits: np.ndarray, w_router: np.ndarray, k: int,
+          bias: Optional[np.ndarray] = None):
+    """Returns (logits fp32 [T][E], topk_ids int32 [T][k], topk_w fp32 [T][k])."""
+    x_bits = np.ascontiguousarray(x_bits, np.uint16)
+    w_router = np.ascontiguousarray(w_router, np.float32)
+    T, d = x_bits.shape
+    E = w_router.shape[0]
+    logits = np.empty((T, E), np.float32)
+    ids = np.empty((T, k), np.int32)
+    w = np.empty((T, k), np.float32)
+    b = None if bias is None else np.ascontiguousarray(bias, np.float32)
+    st = lib().oracle_route(_ptr(x_bits), T, d, _ptr(w_router), _ptr(b), E, k,
+                            _ptr(logits), _ptr(ids), _ptr(w))
+    if st != OK:
+        raise ValueError("oracle_route: status %d" % st)
+    return logits, ids, w
+
+
+def permute(ids: np.ndarray, E: int, S: int):
+    """Returns (offsets [E+S+1], perm_token [T*(k+S)], inv_perm [T][k+S])."""
+    ids = np.ascontiguousarray(ids, np.int32)
+    T, k = ids.shape
+    offsets = np.empty(E + S + 1, np.int32)
+    perm = np.empty(T * (k + S), np.int32)
+    inv = np.empty((T, k + S), np.int32)
+    st = lib().oracle_permute(_ptr(ids), T, E, k, S, _ptr(offsets), _ptr(perm), _ptr(inv))
+    if st != OK:
+        raise ValueError("oracle_permute: status %d" % st)
+    return offsets, perm, inv
+
+
+# ---------------------------------------------------------------------------
+# switch
+# ---------------------------------------------------------------------------
+def switch(hdr: np.ndarray, E: int, R: int, slots_on: Sequence[int]):
+    """Returns (status, row_slot int32 [E][R])."""
+    hdr = np.ascontiguousarray(hdr, np.int32).reshape(-1, 2)
+    on = np.ascontiguousarray(np.asarray(slots_on, np.int32))
+    row_slot = np.empty((E, R), np.int32)
+    st = lib().oracle_switch(_ptr(hdr), hdr.shape[0], E, R, _ptr(on), len(on), _ptr(row_slot))
+    return st, row_slot
+
+
+# ---------------------------------------------------------------------------
+# FFN and combine
+# ---------------------------------------------------------------------------
+def expert_ffn(Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray, x_bits: np.ndarray,
+               rows: np.ndarray, round_h: bool = True) -> np.ndarray:
+    Wg = np.ascontiguousarray(Wg, np.float64)
+    Wu = np.ascontiguousarray(Wu, np.float64)
+    Wd = np.ascontiguousarray(Wd, np.float64)
+    f, d = Wg.shape
+    assert Wu.shape == (f, d) and Wd.shape == (d, f)
+    x_bits = np.ascontiguousarray(x_bits, np.uint16)
+    rows = np.ascontiguousarray(rows, np.int32)
+    out = np.empty((len(rows), d), np.float64)
+    if len(rows):
+        lib().oracle_expert_ffn(_ptr(Wg), _ptr(Wu), _ptr(Wd), f, d, _ptr(x_bits),
+                                _ptr(rows), len(rows), 1 if round_h else 0, _ptr(out))
+    return out
+
+
+def combine(o: np.ndarray, inv: np.ndarray, w: np.ndarray, k: int, S: int) -> np.ndarray:
+    o = np.ascontiguousarray(o, np.float64)
+    inv = np.ascontiguousarray(inv, np.int32)
+    w = np.ascontiguousarray(w, np.float32)
+    T = inv.shape[0]
+    d = o.shape[1]
+    y = np.empty((T, d), np.float64)
+    lib().oracle_combine(_ptr(o), _ptr(inv), _ptr(w), T, k, S, d, _ptr(y))
+    return y
+
+
+def effective_weight(w_fp32: np.ndarray, bits: int, group: int,
+                     switched_rows: Optional[np.ndarray] = None) -> np.ndarray:
+    """Dequantized expert matrix as the FFN sees it: base codes at `bits`,
+    except the switched rows, which read their 8-bit copy quantized from the
+    original fp32 row (Sec. IV-B: the cache keeps the original channels; the
+    copy here is their 8-bit quantization)."""
+    st, q, s, z = quantize(w_fp32, bits, group)
+    if st != OK:
+        raise ValueError("oracle quantize: status %d" % st)
+    W = dequant(q, s, z, group)
+    if switched_rows is not None and len(switched_rows):
+        rows = np.asarray(switched_rows, np.int64)
+        st, q8, s8, z8 = quantize(w_fp32[rows], 8, group)
+        if st != OK:
+            raise ValueError("oracle quantize: status %d" % st)
+        W[rows] = dequant(q8, s8, z8, group)
+    return W
+
+
+def layer_forward(layer, x_bits: np.ndarray, bias: Optional[np.ndarray] = None,
+                  row_slot: Optional[Dict[int, np.ndarray]] = None,
+                  round_h: bool = True, tokens: Optional[np.ndarray] = None,
+                  weight_cache: Optional[dict] = None):
+    """One MoE layer on the CPU.
+
+    layer     moe_inputs.LayerInputs (weights are drawn from it)
+    row_slot  {kind: int32 [E][R]} switch state (-1 = base), or None
+    tokens    optional subset of token indices whose outputs are computed
+              (routing is always done for all tokens)
+    Returns dict with logits, topk_ids, topk_w, offsets, perm, inv and y
+    (y rows for `tokens`, float64).
+    """
+    cfg = layer.cfg
+    E, S, k = cfg.n_experts, cfg.n_shared, cfg.top_k
+    logits, ids, w = route(x_bits, layer.router, k, bias)
+    offsets, perm, inv = permute(ids, E, S)
+    T = x_bits.shape[0]
+    sel = np.arange(T) if tokens is None else np.asarray(tokens)
+    need = np.zeros(T * (k + S), bool)
+    need[inv[sel].ravel()] = True
+    o = np.zeros((T * (k + S), cfg.d_model), np.float64)
+    for e in range(E + S):
+        lo, hi = offsets[e], offsets[e + 1]
+        rows_p = np.arange(lo, hi)[need[lo:hi]]
+        if len(rows_p) == 0:
+            continue
+        Ws = []
+        for kind in (0, 1, 2):
+            key = (e, kind)
+            if weight_cache is not None and key in weight_cache:
+                Ws.append(weight_cache[key])
+                continue
+            sw = None
+            if row_slot is not None and e < E:
+                sw = np.nonzero(row_slot[kind][e] >= 0)[0]
+            W = effective_weight(layer.weight(e, kind), int(layer.bits[e]), cfg.group, sw)
+            if weight_cache is not None:
+                weight_cache[key] = W
+            Ws.append(W)
+        o[rows_p] = expert_ffn(Ws[0], Ws[1], Ws[2], x_bits, perm[rows_p], round_h)
+    y = combine(o, inv[sel], w[sel], k, S)
+    return dict(logits=logits, topk_ids=ids, topk_w=w, offsets=offsets,
+                perm=perm, inv=inv, y=y, tokens=sel)
