@@ -1,0 +1,111 @@
+"""Python names of the C ABI (include/moe_quant.h), taking torch tensors.
+
+torch supplies device memory and the stream only; each function marshals its
+arguments into the matching ``extern "C"`` entry point of libmoe_quant.so and
+raises MoEError on a non-zero status.  Integer bit patterns (packed codes,
+{scale, zero} words) live in int32 tensors; bf16 activations in bfloat16
+tensors.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional, Tuple
+
+import numpy as np
+import torch
+
+from ._lib import LayerDesc, MoEError, check, load
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _s(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise MoEError("expected a device tensor")
+
+
+def moe_quant_pack(w: torch.Tensor, bits: int, group: int, codes: torch.Tensor,
+                   sz: torch.Tensor, n: Optional[int] = None,
+                   rows: Optional[torch.Tensor] = None, ld_codes: Optional[int] = None,
+                   sz_row_stride: Optional[int] = None, sz_group_stride: int = 1,
+                   status: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Quantize rows of fp32 w [R][K] at `bits` and pack them (Sec. IV-A, V-B)."""
+    _need_cuda(w, codes, sz, rows, status)
+    R, K = w.shape
+    n = (R if rows is None else rows.numel()) if n is None else n
+    ld = K * bits // 32 if ld_codes is None else ld_codes
+    srs = K // group if sz_row_stride is None else sz_row_stride
+    st = load().moe_quant_pack(_p(w), w.stride(0), R, K, bits, group, _p(rows), n,
+                               _p(codes), ld, _p(sz), srs, sz_group_stride, _p(status),
+                               _s(stream))
+    check(st, "moe_quant_pack")
+
+
+def moe_route_workspace_bytes(T: int, E: int, k: int, S: int) -> int:
+    return int(load().moe_route_workspace_bytes(T, E, k, S))
+
+
+def moe_route_permute(x: torch.Tensor, w_router: torch.Tensor, bias: Optional[torch.Tensor],
+                      k: int, S: int, topk_ids: torch.Tensor, topk_w: torch.Tensor,
+                      offsets: torch.Tensor, perm_token: torch.Tensor, inv_perm: torch.Tensor,
+                      ws: torch.Tensor, x_perm: Optional[torch.Tensor] = None,
+                      stream=None) -> None:
+    """Router, top-k and permutation into per-expert segments (Sec. II-A)."""
+    _need_cuda(x, w_router, bias, topk_ids, topk_w, offsets, perm_token, inv_perm, ws, x_perm)
+    T, d = x.shape
+    E = w_router.shape[0]
+    st = load().moe_route_permute(_p(x), T, d, _p(w_router), _p(bias), E, k, S, _p(topk_ids),
+                                  _p(topk_w), _p(offsets), _p(perm_token), _p(inv_perm),
+                                  _p(x_perm), _p(ws), ws.numel() * ws.element_size(), _s(stream))
+    check(st, "moe_route_permute")
+
+
+def moe_ffn_plan(desc: LayerDesc, T: int, k: int) -> Tuple[int, int]:
+    ns = C.c_int32(0)
+    wb = C.c_size_t(0)
+    check(load().moe_ffn_plan(C.byref(desc), T, k, C.byref(ns), C.byref(wb)), "moe_ffn_plan")
+    return int(ns.value), int(wb.value)
+
+
+def moe_expert_ffn_mixed(desc: LayerDesc, x: torch.Tensor, k: int, offsets: torch.Tensor,
+                         perm_token: torch.Tensor, o: torch.Tensor, ws: torch.Tensor,
+                         stream=None) -> None:
+    """Grouped mixed-precision SiLU-GLU expert FFN (Sec. IV-A, IV-B, V-B)."""
+    _need_cuda(x, offsets, perm_token, o, ws)
+    T = x.shape[0]
+    st = load().moe_expert_ffn_mixed(C.byref(desc), _p(x), T, k, _p(offsets), _p(perm_token),
+                                     _p(o), _p(ws), ws.numel() * ws.element_size(), _s(stream))
+    check(st, "moe_expert_ffn_mixed")
+
+
+def moe_set_channel_switch(desc: LayerDesc, kind: int, slots_on: Optional[np.ndarray],
+                           stream=None) -> None:
+    """Install cached 8-bit copies by (expert, row) header (Sec. IV-B, V-A)."""
+    if slots_on is None or len(slots_on) == 0:
+        arr, ptr, n = None, None, 0
+    else:
+        arr = np.ascontiguousarray(slots_on, dtype=np.int32)
+        ptr, n = arr.ctypes.data_as(C.c_void_p), int(arr.size)
+    st = load().moe_set_channel_switch(C.byref(desc), kind, ptr, n, _s(stream))
+    check(st, "moe_set_channel_switch")
+
+
+def moe_unpermute_combine(o: torch.Tensor, n_split: int, inv_perm: torch.Tensor,
+                          topk_w: torch.Tensor, k: int, S: int, y: torch.Tensor,
+                          stream=None) -> None:
+    """y[t] = sum_j w[t][j] o[inv[t][j]] + sum_s o[inv[t][k+s]]."""
+    _need_cuda(o, inv_perm, topk_w, y)
+    T, d = y.shape
+    split_stride = o.stride(0) if o.dim() == 3 else o.numel()
+    st = load().moe_unpermute_combine(_p(o), n_split, split_stride, _p(inv_perm), _p(topk_w),
+                                      T, k, S, d, _p(y), _s(stream))
+    check(st, "moe_unpermute_combine")

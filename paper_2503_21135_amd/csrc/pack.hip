@@ -1,0 +1,147 @@
+// pack.hip -- moe_quant_pack: group-wise asymmetric uniform quantization of
+// fp32 rows and packing of the codes into 32-bit words.
+//
+// Sec. IV-A (each expert quantized uniformly at its precision) and Sec. V-B
+// (several low-bit codes loaded as one 32-bit word).  The quantizer and the
+// word layout are defined in moe_quant.h; parameter math is binary64, which
+// gfx950 rounds exactly as IEEE requires, so the codes are reproducible bit
+// for bit on any IEEE host.
+#include "common.hpp"
+
+namespace moe {
+namespace {
+
+// Smallest binary16 >= s for a finite s > 0, by truncating the binary64
+// significand and bumping the last kept bit when anything was cut off.
+// Returns 0x7C00 (+inf) past 65504.
+__device__ uint32_t fp16_ceil_bits(double s) {
+  const uint64_t b = static_cast<uint64_t>(__double_as_longlong(s));
+  const int e = static_cast<int>((b >> 52) & 0x7FF) - 1023;
+  const uint64_t frac = b & ((1ull << 52) - 1);
+  if (e < -24) return 1u;  // below the smallest subnormal 2^-24
+  if (e < -14) {           // subnormal grid k * 2^-24, k = ceil(s * 2^24)
+    const uint64_t full = (1ull << 52) | frac;
+    const int sh = 52 - (e + 24);
+    uint64_t k = full >> sh;
+    if (full & ((1ull << sh) - 1)) k++;
+    return static_cast<uint32_t>(k);  // k == 1024 is the pattern of 2^-14
+  }
+  if (e > 15) return 0x7C00u;
+  uint32_t h = static_cast<uint32_t>(((e + 15) << 10) | (frac >> 42));
+  if (frac & ((1ull << 42) - 1)) h++;  // may carry into the exponent, up to +inf
+  return h;
+}
+
+// Value of an fp16 bit pattern as binary64 (exact).
+__device__ double fp16_to_f64(uint32_t h) { return static_cast<double>(fp16_bits_to_f32(h)); }
+
+// binary16 pattern of an integer 0 <= z <= 255 (exact).
+__device__ uint32_t fp16_of_small_int(int z) {
+  return __builtin_bit_cast(uint16_t, static_cast<_Float16>(static_cast<float>(z)));
+}
+
+// Bit position of local code i in a word of the b-bit half-split order.
+__device__ __forceinline__ int hs_pos(int i, int b) { return (i >> 1) * b + 16 * (i & 1); }
+
+// One thread per (list row, group).
+__global__ void __launch_bounds__(256)
+pack_kernel(const float* __restrict__ w, int64_t ld_w, int K, int bits, int group,
+            const int32_t* __restrict__ rows, int n, uint32_t* __restrict__ codes,
+            int64_t ld_codes, uint32_t* __restrict__ sz, int64_t sz_rs, int64_t sz_gs,
+            int32_t* status) {
+  const int G = K / group;
+  const int64_t id = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (id >= static_cast<int64_t>(n) * G) return;
+  const int i = static_cast<int>(id / G);
+  const int j = static_cast<int>(id % G);
+  const int r = rows ? rows[i] : i;
+  const float* wg = w + static_cast<int64_t>(r) * ld_w + static_cast<int64_t>(j) * group;
+
+  double mn = 0.0, mx = 0.0;
+  for (int c = 0; c < group; c++) {
+    const double v = static_cast<double>(wg[c]);
+    mn = v < mn ? v : mn;
+    mx = v > mx ? v : mx;
+  }
+  const int qmax = (1 << bits) - 1;
+  const double s = (mx - mn) / static_cast<double>(qmax);
+  const uint32_t sb = (s == 0.0) ? 0x3C00u : fp16_ceil_bits(s);
+  if (sb == 0x7C00u && status) *status = MOE_ERR_RANGE;
+  const double sf = fp16_to_f64(sb);
+  int z = static_cast<int>(rint(-mn / sf));
+  z = z < 0 ? 0 : z;
+  sz[static_cast<int64_t>(i) * sz_rs + static_cast<int64_t>(j) * sz_gs] =
+      sb | (fp16_of_small_int(z) << 16);
+
+  auto code = [&](int c) -> uint32_t {
+    double t = rint(static_cast<double>(wg[c]) / sf) + static_cast<double>(z);
+    t = t < 0.0 ? 0.0 : (t > static_cast<double>(qmax) ? static_cast<double>(qmax) : t);
+    return static_cast<uint32_t>(t);
+  };
+
+  uint32_t* out = codes + static_cast<int64_t>(i) * ld_codes +
+                  static_cast<int64_t>(j) * (group * bits / 32);
+  if (bits != 3) {
+    const int per = 32 / bits;
+    for (int t = 0; t < group / per; t++) {
+      uint32_t word = 0;
+      for (int l = 0; l < per; l++) word |= code(t * per + l) << hs_pos(l, bits);
+      out[t] = word;
+    }
+  } else {
+    for (int blk = 0; blk < group / 32; blk++) {
+      uint32_t lo0 = 0, lo1 = 0, hi = 0;
+      for (int l = 0; l < 32; l++) {
+        const uint32_t q = code(blk * 32 + l);
+        if (l < 16)
+          lo0 |= (q & 3u) << hs_pos(l, 2);
+        else
+          lo1 |= (q & 3u) << hs_pos(l - 16, 2);
+        hi |= ((q >> 2) & 1u) << hs_pos(l, 1);
+      }
+      out[3 * blk] = lo0;
+      out[3 * blk + 1] = lo1;
+      out[3 * blk + 2] = hi;
+    }
+  }
+}
+
+}  // namespace
+}  // namespace moe
+
+extern "C" int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K,
+                              int32_t bits, int32_t group, const int32_t* rows, int32_t n,
+                              uint32_t* codes, int64_t ld_codes, uint32_t* sz,
+                              int64_t sz_row_stride, int64_t sz_group_stride,
+                              int32_t* status, void* stream) {
+  using namespace moe;
+  if (!valid_bits(bits)) return MOE_ERR_BITS;
+  if (!w || !codes || !sz || R <= 0 || K <= 0 || n < 0) return MOE_ERR_ARG;
+  if (!(group == 64 || group == 128) || K % group || K % 32) return MOE_ERR_ARG;
+  if (bits == 3 && group != 128) return MOE_ERR_ARG;
+  if (ld_w < K || ld_codes < static_cast<int64_t>(K) * bits / 32) return MOE_ERR_ARG;
+  if (!rows && n > R) return MOE_ERR_ARG;
+  if (!aligned16(codes) || (ld_codes * 4) % 16) return MOE_ERR_ALIGN;
+  if (n == 0) return MOE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t total = static_cast<int64_t>(n) * (K / group);
+  const int threads = 256;
+  hipLaunchKernelGGL(pack_kernel, dim3(static_cast<unsigned>(cdiv(total, threads))),
+                     dim3(threads), 0, s, w, ld_w, K, bits, group, rows, n, codes, ld_codes,
+                     sz, sz_row_stride, sz_group_stride, status);
+  return launch_status(s);
+}
+
+extern "C" const char* moe_status_str(int status) {
+  switch (status) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_ARG: return "invalid argument";
+    case MOE_ERR_BITS: return "bit-width not in {2,3,4,8}";
+    case MOE_ERR_ALIGN: return "pointer or stride not 16-byte aligned";
+    case MOE_ERR_WORKSPACE: return "workspace missing or too small";
+    case MOE_ERR_SLOT: return "bad switch slot list";
+    case MOE_ERR_RANGE: return "fp16 scale overflow";
+    case MOE_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}

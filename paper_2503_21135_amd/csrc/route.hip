@@ -1,0 +1,268 @@
+// route.hip -- moe_route_permute: router logits, top-k selection, combine
+// weights and the permutation of token rows into per-expert segments.
+//
+// Sec. II-A: a fixed number k of experts is selected per token.  The token ->
+// several experts mapping (Sec. I, Sec. II-A "Data-Weight Mappings") becomes
+// a histogram of expert choices, an exclusive scan into segment offsets and a
+// stable scatter of token indices.  Everything is bitwise reproducible: the
+// logit reduction order is fixed (moe_quant.h), the exponential is the
+// library's own, and the permutation uses no atomics.
+#include "common.hpp"
+
+#pragma clang fp contract(off)
+
+namespace moe {
+namespace {
+
+constexpr int kChunk = 64;  // tokens per histogram chunk (one wave)
+
+// Exponential for x <= 0 as the header defines it: Cody-Waite reduction by
+// ln2 split into 2839/4096 (12 significant bits) and its fp32 remainder,
+// Taylor polynomial of degree 7 in Horner form, scaling by 2^n.
+__device__ float lib_exp_nonpos(float x) {
+  if (x < -80.0f) return 0.0f;
+  constexpr float kLog2e = static_cast<float>(1.4426950408889634);
+  constexpr float kLn2Hi = 2839.0f / 4096.0f;
+  constexpr float kLn2Lo = static_cast<float>(0.69314718055994531 - 2839.0 / 4096.0);
+  constexpr float kC[8] = {static_cast<float>(1.0),
+                           static_cast<float>(1.0),
+                           static_cast<float>(1.0 / 2.0),
+                           static_cast<float>(1.0 / 6.0),
+                           static_cast<float>(1.0 / 24.0),
+                           static_cast<float>(1.0 / 120.0),
+                           static_cast<float>(1.0 / 720.0),
+                           static_cast<float>(1.0 / 5040.0)};
+  const float n = rintf(x * kLog2e);
+  float r = __fmaf_rn(-n, kLn2Hi, x);
+  r = __fmaf_rn(-n, kLn2Lo, r);
+  float p = kC[7];
+#pragma unroll
+  for (int i = 6; i >= 0; i--) p = __fmaf_rn(p, r, kC[i]);
+  return ldexpf(p, static_cast<int>(n));
+}
+
+// Wave-wide reduction of the 64 lane partials; lane 0 ends with the value of
+// the header's halving tree (partial[l] += partial[l ^ off] pairs exactly the
+// tree's operands at lane 0).
+__device__ __forceinline__ float tree_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = v + __shfl_xor(v, off, kWave);
+  return __shfl(v, 0, kWave);
+}
+
+// One wave per token: logits, top-k, weights.
+__global__ void __launch_bounds__(256)
+route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
+                  const float* __restrict__ bias, int E, int k,
+                  int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const uint16_t* xr = x + static_cast<int64_t>(t) * d;
+  constexpr int kMaxPer = MOE_MAX_EXPERTS / kWave;
+  float lg[kMaxPer];
+#pragma unroll
+  for (int m = 0; m < kMaxPer; m++) lg[m] = -INFINITY;
+  for (int e = 0; e < E; e++) {
+    const float* we = wr + static_cast<int64_t>(e) * d;
+    float acc = 0.0f;
+    for (int c = lane; c < d; c += kWave)
+      acc = __fmaf_rn(__uint_as_float(static_cast<uint32_t>(xr[c]) << 16), we[c], acc);
+    float v = tree_sum(acc);
+    if (bias) v = v + bias[e];
+#pragma unroll
+    for (int m = 0; m < kMaxPer; m++)
+      if (e == m * kWave + lane) lg[m] = v;
+  }
+  // top-k by (logit desc, index asc); every lane ends with the same picks
+  uint64_t taken[kMaxPer];
+  int ids[MOE_MAX_TOPK];
+  float sel[MOE_MAX_TOPK];
+#pragma unroll
+  for (int m = 0; m < kMaxPer; m++) taken[m] = 0;
+  for (int j = 0; j < k; j++) {
+    float bv = -INFINITY;
+    int bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int m = 0; m < kMaxPer; m++) {
+      const int e = m * kWave + lane;
+      if (e < E && !taken[m] && (lg[m] > bv || (lg[m] == bv && e < bi))) {
+        bv = lg[m];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float ov = __shfl_xor(bv, off, kWave);
+      const int oi = __shfl_xor(bi, off, kWave);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    ids[j] = bi;
+    sel[j] = bv;
+#pragma unroll
+    for (int m = 0; m < kMaxPer; m++)
+      if (bi == m * kWave + lane) taken[m] = 1;
+  }
+  if (lane == 0) {
+    float ex[MOE_MAX_TOPK];
+    const float mref = sel[0];
+    float S = 0.0f;
+    for (int j = 0; j < k; j++) {
+      ex[j] = lib_exp_nonpos(sel[j] - mref);
+      S = S + ex[j];
+    }
+    for (int j = 0; j < k; j++) {
+      topk_ids[static_cast<int64_t>(t) * k + j] = ids[j];
+      topk_w[static_cast<int64_t>(t) * k + j] = ex[j] / S;
+    }
+  }
+}
+
+// hist[c][e] = number of tokens of chunk c that selected e.
+__global__ void __launch_bounds__(64)
+route_hist_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k,
+                  int32_t* __restrict__ hist) {
+  const int c = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int t = c * kChunk + lane;
+  int mine[MOE_MAX_TOPK];
+  for (int j = 0; j < k; j++) mine[j] = (t < T) ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
+  for (int e = 0; e < E; e++) {
+    bool has = false;
+    for (int j = 0; j < k; j++) has |= (mine[j] == e);
+    const uint64_t m = __ballot(has);
+    if (lane == 0) hist[static_cast<int64_t>(c) * E + e] = __popcll(m);
+  }
+}
+
+// offsets[] and per-chunk segment bases (single workgroup; one thread per
+// expert column, chunks in order).
+__global__ void __launch_bounds__(256)
+route_scan_kernel(const int32_t* __restrict__ hist, int n_chunks, int T, int E, int k, int S,
+                  int32_t* __restrict__ base, int32_t* __restrict__ offsets) {
+  __shared__ int32_t tot[MOE_MAX_EXPERTS];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int s = 0;
+    for (int c = 0; c < n_chunks; c++) {
+      base[static_cast<int64_t>(c) * E + e] = s;
+      s += hist[static_cast<int64_t>(c) * E + e];
+    }
+    tot[e] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int e = 0; e < E; e++) {
+      offsets[e] = acc;
+      acc += tot[e];
+    }
+    for (int s2 = 0; s2 <= S; s2++) offsets[E + s2] = acc + s2 * T;
+  }
+}
+
+// Stable scatter: rank of a token inside its chunk's share of segment e is
+// the number of earlier lanes of the chunk that selected e.
+__global__ void __launch_bounds__(64)
+route_scatter_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k, int S,
+                     const int32_t* __restrict__ base, const int32_t* __restrict__ offsets,
+                     int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_perm) {
+  const int c = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int t = c * kChunk + lane;
+  const bool live = t < T;
+  int mine[MOE_MAX_TOPK];
+  int pos[MOE_MAX_TOPK];
+  for (int j = 0; j < k; j++) {
+    mine[j] = live ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
+    pos[j] = -1;
+  }
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int e = 0; e < E; e++) {
+    bool has = false;
+    for (int j = 0; j < k; j++) has |= (mine[j] == e);
+    const uint64_t m = __ballot(has);
+    if (!m) continue;
+    if (has) {
+      const int p = offsets[e] + base[static_cast<int64_t>(c) * E + e] + __popcll(m & below);
+      for (int j = 0; j < k; j++)
+        if (mine[j] == e) pos[j] = p;
+    }
+  }
+  if (!live) return;
+  const int64_t row = static_cast<int64_t>(t) * (k + S);
+  for (int j = 0; j < k; j++) {
+    perm_token[pos[j]] = t;
+    inv_perm[row + j] = pos[j];
+  }
+  for (int s = 0; s < S; s++) {
+    const int p = offsets[E + s] + t;
+    perm_token[p] = t;
+    inv_perm[row + k + s] = p;
+  }
+}
+
+// x_perm[p] = x[perm_token[p]] (16-byte copies; d % 8 == 0).
+__global__ void __launch_bounds__(256)
+gather_rows_kernel(const uint16_t* __restrict__ x, int d, const int32_t* __restrict__ perm_token,
+                   int rows, uint16_t* __restrict__ x_perm) {
+  const int per_row = d / 8;
+  const int64_t id = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (id >= static_cast<int64_t>(rows) * per_row) return;
+  const int64_t p = id / per_row;
+  const int q = static_cast<int>(id % per_row);
+  const u32x4* src = reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(perm_token[p]) * d) + q;
+  reinterpret_cast<u32x4*>(x_perm + p * d)[q] = *src;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+}  // namespace
+}  // namespace moe
+
+extern "C" size_t moe_route_workspace_bytes(int32_t T, int32_t E, int32_t k, int32_t S) {
+  (void)k;
+  (void)S;
+  if (T < 0 || E <= 0) return 0;
+  const size_t n_chunks = static_cast<size_t>((T + moe::kChunk - 1) / moe::kChunk);
+  return 2 * moe::align256(sizeof(int32_t) * (n_chunks > 0 ? n_chunks : 1) * E);
+}
+
+extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const float* w_router,
+                                 const float* bias, int32_t E, int32_t k, int32_t S,
+                                 int32_t* topk_ids, float* topk_w, int32_t* offsets,
+                                 int32_t* perm_token, int32_t* inv_perm, uint16_t* x_perm,
+                                 void* ws, size_t ws_bytes, void* stream) {
+  using namespace moe;
+  if (T < 0 || d <= 0 || d % 64 || E <= 0 || S < 0 || E + S > MOE_MAX_EXPERTS) return MOE_ERR_ARG;
+  if (k < 1 || k > E || k > MOE_MAX_TOPK) return MOE_ERR_ARG;
+  if (!offsets || (T > 0 && (!x || !w_router || !topk_ids || !topk_w || !perm_token || !inv_perm)))
+    return MOE_ERR_ARG;
+  if (x_perm && (!aligned16(x_perm) || !aligned16(x))) return MOE_ERR_ALIGN;
+  const size_t need = moe_route_workspace_bytes(T, E, k, S);
+  if (!ws || ws_bytes < need) return MOE_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n_chunks = static_cast<int>(cdiv(T, kChunk));
+  int32_t* hist = static_cast<int32_t*>(ws);
+  int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + need / 2);
+  if (T > 0) {
+    hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(cdiv(T, 4))), dim3(256), 0, s,
+                       x, T, d, w_router, bias, E, k, topk_ids, topk_w);
+    hipLaunchKernelGGL(route_hist_kernel, dim3(n_chunks), dim3(64), 0, s, topk_ids, T, E, k, hist);
+  }
+  hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(256), 0, s, hist, n_chunks, T, E, k, S,
+                     base, offsets);
+  if (T > 0) {
+    hipLaunchKernelGGL(route_scatter_kernel, dim3(n_chunks), dim3(64), 0, s, topk_ids, T, E, k, S,
+                       base, offsets, perm_token, inv_perm);
+    if (x_perm) {
+      const int64_t rows = static_cast<int64_t>(T) * (k + S);
+      const int64_t n = rows * (d / 8);
+      hipLaunchKernelGGL(gather_rows_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256),
+                         0, s, x, d, perm_token, static_cast<int>(rows), x_perm);
+    }
+  }
+  return launch_status(s);
+}
