@@ -1,0 +1,271 @@
+#!/usr/bin/env python3
+"""Benchmark of the mixed-precision MoE-layer hot path on one MI355X.
+
+A step is one pass of the whole path over one batch already resident in HBM:
+moe_route_permute -> moe_expert_ffn_mixed -> moe_unpermute_combine.
+Default workload: the Mixtral-8x7B-shaped layer at decode (64 tokens,
+d_model 4096, 8 experts, top-2, d_ff 14336, group 128, expert bits
+{8:2, 4:4, 2:2}, 5 % of output channels switched to resident 8-bit copies).
+
+Prints one JSON line with tokens/s, the roofline of the dominant kernel (the
+gate/up expert kernel, timed with HIP events on its own stream) and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles created through the HIP runtime torch already loaded."""
+
+    def __init__(self):
+        self.hip = C.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.hip.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def create(self, n):
+        arr = (C.c_void_p * n)()
+        for i in range(n):
+            ev = C.c_void_p()
+            if self.hip.hipEventCreate(C.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            arr[i] = ev.value
+        return arr
+
+    def record(self, ev, stream):
+        if self.hip.hipEventRecord(C.c_void_p(ev), C.c_void_p(stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def ms(self, a, b):
+        out = C.c_float()
+        if self.hip.hipEventElapsedTime(C.byref(out), C.c_void_p(a), C.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(out.value)
+
+    def destroy(self, arr):
+        for v in arr:
+            self.hip.hipEventDestroy(C.c_void_p(v))
+
+
+def algorithmic_bytes(layer, offsets):
+    """Packed-weight bytes one step must read, per FFN stage: base codes of
+    unswitched rows, 8-bit copy codes of switched rows and one {scale, zero}
+    word per row and group, over the experts that received tokens."""
+    cfg = layer.cfg
+    E, S, g = layer.E, layer.S, cfg.group
+    counts = np.diff(offsets)
+    out = {"gate_up": 0, "down": 0}
+    for e in range(E + S):
+        if counts[e] == 0:
+            continue
+        b = int(layer.bits_host[e])
+        for kind in range(3):
+            R, K = cfg.rows(kind, e), cfg.cols(kind, e)
+            n_sw = int(np.sum(layer.row_slot(kind)[e] >= 0)) if e < E else 0
+            nb = (R - n_sw) * K * b // 8 + n_sw * K + R * (K // g) * 4
+            out["down" if kind == 2 else "gate_up"] += nb
+    return out
+
+
+def algorithmic_flops(layer, offsets):
+    cfg = layer.cfg
+    counts = np.diff(offsets)
+    fl = 0
+    for e in range(layer.E + layer.S):
+        f = cfg.d_ff if e < layer.E else cfg.d_ff_shared
+        fl += int(counts[e]) * 2 * 3 * cfg.d_model * f
+    return fl
+
+
+def describe(wk):
+    c = wk.layer
+    bits = dict(c.bit_shares) if c.bit_shares else list(c.bits_literal)
+    d = {"workload": "%s: %s, T=%d" % (wk.name, c.name, wk.tokens), "tokens": wk.tokens,
+         "d_model": c.d_model, "experts": c.n_experts, "shared_experts": c.n_shared,
+         "top_k": c.top_k, "d_ff": c.d_ff, "group": c.group, "bits": str(bits),
+         "switched_rows": "%s %s" % (c.copies, c.mask_frac if c.copies != "pool" else c.pool_frac)}
+    if c.n_shared:
+        d["d_ff_shared"] = c.d_ff_shared
+    if wk.zipf_s:
+        d["router_zipf_s"] = wk.zipf_s
+    return d
+
+
+def cpu_baseline(wk, inputs, batch, n_tok):
+    import oracle
+    rs = oracle.switch_state(inputs, epoch=0)
+    toks = np.arange(min(n_tok, wk.tokens))
+    t0 = time.perf_counter()
+    oracle.layer_forward(inputs, batch.x, bias=batch.bias, row_slot=rs, tokens=toks)
+    dt = time.perf_counter() - t0
+    return {"value": round(len(toks) / dt, 4), "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": "%d of %d tokens of the same batch: router for all tokens, "
+                      "quantize+dequantize of every expert those tokens reach, fp64 FFN, "
+                      "combine (%.1f s)" % (len(toks), wk.tokens, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="mixtral-decode")
+    ap.add_argument("--cpu-tokens", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run 10 plain device-to-device copies of MIB MiB (the "
+                         "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
+    args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        b = torch.empty_like(a)
+        for _ in range(10):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log("copied %d MiB x 10" % args.copy_calibration)
+        return
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import moe_inputs as mi
+    import paper_2503_21135_amd as P
+    from paper_2503_21135_amd import api
+
+    wk = mi.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    t_build = time.perf_counter()
+    inputs = mi.LayerInputs(wk.layer)
+    layer = P.MoELayer(inputs, device="cuda:0")
+    layer.set_epoch(0)
+    batch = mi.make_batch(wk, inputs)
+    x = torch.from_numpy(batch.x.view(np.int16)).to(dev).view(torch.bfloat16)
+    bias = None if batch.bias is None else torch.from_numpy(batch.bias).to(dev)
+    torch.cuda.synchronize()
+    log("layer packed in %.1f s; packed bytes %.1f MB" %
+        (time.perf_counter() - t_build, layer.packed_bytes() / 1e6))
+
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+    hip = HipEvents()
+    K, W = args.steps, args.warmup
+    n_stage = 5
+    ev_ffn = hip.create(n_stage * K)
+    ev_edge = hip.create(2 * K)
+    b = layer.buffers(wk.tokens)
+
+    def step(i=None):
+        layer.route(x, bias)
+        if i is None:
+            layer.ffn(x, b)
+        else:
+            evs = (C.c_void_p * n_stage)(*ev_ffn[i * n_stage:(i + 1) * n_stage])
+            api.moe_expert_ffn_mixed_ev(layer.desc, x, layer.k, b.offsets, b.perm, b.o,
+                                        b.ffn_ws, evs)
+        layer.combine(b)
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    offsets = b.offsets.cpu().numpy()
+
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for i in range(K):
+        hip.record(ev_edge[2 * i], sptr)
+        step(i)
+        hip.record(ev_edge[2 * i + 1], sptr)
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / K
+
+    stages = np.zeros((K, n_stage - 1))
+    for i in range(K):
+        e = ev_ffn[i * n_stage:(i + 1) * n_stage]
+        stages[i] = [hip.ms(e[j], e[j + 1]) for j in range(n_stage - 1)]
+    layer_ms = np.array([hip.ms(ev_edge[2 * i], ev_edge[2 * i + 1]) for i in range(K)])
+    st = stages.mean(0)
+    hip.destroy(ev_ffn)
+    hip.destroy(ev_edge)
+
+    byt = algorithmic_bytes(layer, offsets)
+    flops = algorithmic_flops(layer, offsets)
+    gu_ms = float(st[1])
+    ffn_ms = float(stages.sum(1).mean())
+    achieved = byt["gate_up"] / (gu_ms * 1e-3) / 1e9
+    ffn_gbs = (byt["gate_up"] + byt["down"]) / (ffn_ms * 1e-3) / 1e9
+    tokens_per_s = wk.tokens / (ms_per_step * 1e-3)
+    log("ms/step %.4f (wall %.4f); stages ms: xsum %.4f gate/up %.4f hsum %.4f down %.4f"
+        % (ms_per_step, wall / K * 1e3, *st))
+    log("gate/up %.1f GB/s; FFN %.1f GB/s; %.2f TFLOP/s" %
+        (achieved, ffn_gbs, flops / (ffn_ms * 1e-3) / 1e12))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on %d tokens ..." % args.cpu_tokens)
+        cpu = cpu_baseline(wk, inputs, batch, args.cpu_tokens)
+        log("cpu baseline", cpu)
+
+    bound = "hbm"
+    roof = {"bound": bound, "kernel": "ffn_stream_kernel<NK=2> (gate+up expert projections, "
+                                      "SiLU-GLU epilogue)",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": int(byt["gate_up"]),
+            "avg_launch_ms": round(gu_ms, 5)}
+    out = {
+        "metric": "MoE-layer tokens/sec at decode & prefill; HBM GB/s / MFMA util vs peak",
+        "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) bf16 activations with outlier "
+                "columns)",
+        "config": describe(wk),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "detail": {
+            "layer_ms_events": round(float(layer_ms.mean()), 5),
+            "stage_ms": {"xsum": round(float(st[0]), 5), "gate_up": round(float(st[1]), 5),
+                         "hsum": round(float(st[2]), 5), "down": round(float(st[3]), 5)},
+            "ffn_ms": round(ffn_ms, 5),
+            "ffn_weight_bytes": int(byt["gate_up"] + byt["down"]),
+            "ffn_gbs": round(ffn_gbs, 1), "ffn_hbm_frac": round(ffn_gbs / HBM_PEAK_GBS, 4),
+            "ffn_tflops": round(flops / (ffn_ms * 1e-3) / 1e12, 3),
+            "ffn_mfma_frac": round(flops / (ffn_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5),
+            "wall_ms_per_step": round(wall / K * 1e3, 5),
+            "expert_rows": [int(v) for v in np.diff(offsets)],
+        },
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

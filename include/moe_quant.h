@@ -88,7 +88,7 @@ extern "C" {
 #define MOE_ERR_HIP       -7  /* a HIP call or kernel launch failed                    */
 
 /* Limits checked by the host validation. */
-#define MOE_MAX_EXPERTS  512  /* routed + shared experts of one layer */
+#define MOE_MAX_EXPERTS  256  /* routed + shared experts of one layer */
 #define MOE_MAX_TOPK      16
 
 /* Kinds of expert weight matrix. */
@@ -138,8 +138,10 @@ typedef struct moe_kind_desc {
  *
  * order_gu[e*d_ff + i] and order_dn[e*d_model + i] (routed experts only) are
  * the orders in which the FFN visits hidden neurons and output channels.  They
- * are rebuilt by moe_set_channel_switch so that neurons (channels) with the
- * same precision sources are adjacent; any permutation gives the same result.
+ * are rebuilt by moe_set_channel_switch as stable partitions: first the rows
+ * whose sources are all base codes (n_base[e] of them for gate/up neurons,
+ * n_base[E + e] for down channels), then the rows reading a cached copy.
+ * Any permutation gives the same result.
  */
 typedef struct moe_layer {
   int32_t n_experts;     /* E, routed  */
@@ -153,6 +155,7 @@ typedef struct moe_layer {
   moe_kind_desc_t kind[3];
   int32_t* order_gu;          /* device [E][d_ff]    */
   int32_t* order_dn;          /* device [E][d_model] */
+  int32_t* n_base;            /* device [2][E]: leading base-only rows of the orders */
   int32_t* staging;           /* device scratch of at least max(kind[].n_slots)+1 int32 */
 } moe_layer_t;
 
@@ -211,7 +214,8 @@ int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K,
  *             (t, shared expert s) at j = k+s.
  *   x_perm    device bf16 [T*(k+S)][d] or NULL: x[perm_token[p]] (bit copy).
  *   ws        device workspace of at least moe_route_workspace_bytes(T,E,k,S).
- *   Requires d % 64 == 0, 1 <= k <= min(E, MOE_MAX_TOPK), E+S <= MOE_MAX_EXPERTS.
+ *   Requires d % 64 == 0, d <= 8192, 1 <= k <= min(E, MOE_MAX_TOPK),
+ *   E+S <= MOE_MAX_EXPERTS.
  *   Results are bitwise reproducible.
  */
 int moe_route_permute(const uint16_t* x, int32_t T, int32_t d,
@@ -259,6 +263,23 @@ int moe_expert_ffn_mixed(const moe_layer_t* L, const uint16_t* x, int32_t T,
                          void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * moe_expert_ffn_mixed_ev -- moe_expert_ffn_mixed that also records HIP
+ * events on `stream` at its stage boundaries, so a caller can time each
+ * kernel of the FFN on the stream it runs on.  Not on the hot path of a
+ * production caller; same arguments, results and errors otherwise.
+ *   events    host array of n_events hipEvent_t handles (as void*), each
+ *             created by the caller; NULL entries are skipped:
+ *             [0] before the first launch, [1] after the activation group
+ *             sums, [2] after the gate/up kernels, [3] after the hidden-
+ *             activation group sums, [4] after the down kernels.
+ */
+int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
+                            int32_t k, const int32_t* offsets,
+                            const int32_t* perm_token, float* o,
+                            void* ws, size_t ws_bytes, void* stream,
+                            void* const* events, int32_t n_events);
+
+/*
  * moe_set_channel_switch -- install a set of cached 8-bit copies.
  * Sec. IV-B "Channel Weights Replacement based on Caching" and Sec. V-A "Data
  * Format in the Channel Cache": the copy of each listed slot replaces the row
@@ -268,7 +289,8 @@ int moe_expert_ffn_mixed(const moe_layer_t* L, const uint16_t* x, int32_t T,
  *   kind      MOE_KIND_GATE/UP/DOWN, or -1 with n_on == 0 to reset all kinds.
  *   slots_on  host int32 list of n_on distinct slots in [0, n_slots) whose
  *             headers name distinct rows; copied before the call returns.
- *   Rewrites kind[kind].row_slot and order_gu (gate/up) or order_dn (down).
+ *   Rewrites kind[kind].row_slot, order_gu and n_base[0..E) (gate/up) or
+ *   order_dn and n_base[E..2E) (down).
  */
 int moe_set_channel_switch(moe_layer_t* L, int32_t kind,
                            const int32_t* slots_on, int32_t n_on, void* stream);

@@ -65,6 +65,7 @@ def lib():
             "oracle_switch": (i32, [vp, i32, i32, i32, vp, i32, vp]),
             "oracle_expert_ffn": (None, [vp, vp, vp, i32, i32, vp, vp, i32, i32, vp]),
             "oracle_combine": (None, [vp, vp, vp, i32, i32, i32, i32, vp]),
+            "oracle_num_threads": (i32, []),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -72,6 +73,10 @@ def lib():
             fn.argtypes = args
         _lib = L
     return _lib
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())
 
 
 # ---------------------------------------------------------------------------
@@ -192,6 +197,19 @@ def switch(hdr: np.ndarray, E: int, R: int, slots_on: Sequence[int]):
     row_slot = np.empty((E, R), np.int32)
     st = lib().oracle_switch(_ptr(hdr), hdr.shape[0], E, R, _ptr(on), len(on), _ptr(row_slot))
     return st, row_slot
+
+
+def switch_state(layer, epoch: int = 0, kinds=(0, 1, 2)) -> Dict[int, np.ndarray]:
+    """row_slot tables {kind: [E][R]} of a layer's mask epoch."""
+    cfg = layer.cfg
+    out = {}
+    for kind in kinds:
+        st, rs = switch(layer.copy_headers(kind), cfg.n_experts, cfg.rows(kind, 0),
+                        layer.slots_on(kind, epoch))
+        if st != OK:
+            raise ValueError("oracle switch: status %d" % st)
+        out[kind] = rs
+    return out
 
 
 # ---------------------------------------------------------------------------

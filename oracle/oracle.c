@@ -18,6 +18,9 @@
  * or brute force.  See the header comment of the tests for the list.
  */
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -27,6 +30,15 @@
 #define ORC_ERR_BITS (-2)
 #define ORC_ERR_SLOT (-5)
 #define ORC_ERR_RANGE (-6)
+
+/* Threads the OpenMP loops below use. */
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------ */
 /* 16-bit float formats, written from the IEEE 754 definitions.             */

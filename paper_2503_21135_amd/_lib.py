@@ -14,13 +14,13 @@ LIB_PATH = os.path.join(HERE, "libmoe_quant.so")
 OK, ERR_ARG, ERR_BITS, ERR_ALIGN, ERR_WORKSPACE, ERR_SLOT, ERR_RANGE, ERR_HIP = (
     0, -1, -2, -3, -4, -5, -6, -7)
 KIND_GATE, KIND_UP, KIND_DOWN = 0, 1, 2
-MAX_EXPERTS = 512
+MAX_EXPERTS = 256
 MAX_TOPK = 16
 
 EXPORTS = (
     "moe_quant_pack", "moe_route_permute", "moe_route_workspace_bytes", "moe_ffn_plan",
-    "moe_expert_ffn_mixed", "moe_set_channel_switch", "moe_unpermute_combine",
-    "moe_status_str",
+    "moe_expert_ffn_mixed", "moe_expert_ffn_mixed_ev", "moe_set_channel_switch",
+    "moe_unpermute_combine", "moe_status_str",
 )
 
 
@@ -39,7 +39,8 @@ class LayerDesc(C.Structure):
         ("n_experts", C.c_int32), ("n_shared", C.c_int32), ("d_model", C.c_int32),
         ("d_ff", C.c_int32), ("d_ff_shared", C.c_int32), ("group", C.c_int32),
         ("bits_host", C.c_void_p), ("bits", C.c_void_p), ("kind", KindDesc * 3),
-        ("order_gu", C.c_void_p), ("order_dn", C.c_void_p), ("staging", C.c_void_p),
+        ("order_gu", C.c_void_p), ("order_dn", C.c_void_p), ("n_base", C.c_void_p),
+        ("staging", C.c_void_p),
     ]
 
 
@@ -68,6 +69,8 @@ def load() -> C.CDLL:
         "moe_ffn_plan": (C.c_int, [C.POINTER(LayerDesc), i32, i32, C.POINTER(i32), C.POINTER(sz_t)]),
         "moe_expert_ffn_mixed": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
                                            sz_t, vp]),
+        "moe_expert_ffn_mixed_ev": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
+                                              sz_t, vp, vp, i32]),
         "moe_set_channel_switch": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i32, vp]),
         "moe_unpermute_combine": (C.c_int, [vp, i32, i64, vp, vp, i32, i32, i32, i32, vp, vp]),
         "moe_status_str": (C.c_char_p, [C.c_int]),

@@ -87,6 +87,19 @@ def moe_expert_ffn_mixed(desc: LayerDesc, x: torch.Tensor, k: int, offsets: torc
     check(st, "moe_expert_ffn_mixed")
 
 
+def moe_expert_ffn_mixed_ev(desc: LayerDesc, x: torch.Tensor, k: int, offsets: torch.Tensor,
+                            perm_token: torch.Tensor, o: torch.Tensor, ws: torch.Tensor,
+                            events, stream=None) -> None:
+    """moe_expert_ffn_mixed recording caller-created hipEvent_t handles
+    (a ctypes c_void_p array) at its stage boundaries."""
+    _need_cuda(x, offsets, perm_token, o, ws)
+    T = x.shape[0]
+    st = load().moe_expert_ffn_mixed_ev(C.byref(desc), _p(x), T, k, _p(offsets), _p(perm_token),
+                                        _p(o), _p(ws), ws.numel() * ws.element_size(), _s(stream),
+                                        C.cast(events, C.c_void_p), len(events))
+    check(st, "moe_expert_ffn_mixed_ev")
+
+
 def moe_set_channel_switch(desc: LayerDesc, kind: int, slots_on: Optional[np.ndarray],
                            stream=None) -> None:
     """Install cached 8-bit copies by (expert, row) header (Sec. IV-B, V-A)."""

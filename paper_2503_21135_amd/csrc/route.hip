@@ -50,36 +50,48 @@ __device__ __forceinline__ float tree_sum(float v) {
   return __shfl(v, 0, kWave);
 }
 
-// One wave per token: logits, top-k, weights.
+constexpr int kMaxD = 8192;   // d_model limit of the router (x row staged in LDS)
+
+// One workgroup (4 waves) per token.  The token's activations are staged in
+// LDS as fp32; wave w computes the logits of experts w, w+4, ... with the
+// header's fixed order; wave 0 then selects the top k and forms the weights.
 __global__ void __launch_bounds__(256)
 route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
                   const float* __restrict__ bias, int E, int k,
                   int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
+  __shared__ float xs[kMaxD];
+  __shared__ float lgs[MOE_MAX_EXPERTS];
+  const int t = blockIdx.x;
   const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x >> 6);
-  if (t >= T) return;
+  const int wv = threadIdx.x >> 6;
   const uint16_t* xr = x + static_cast<int64_t>(t) * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x)
+    xs[c] = __uint_as_float(static_cast<uint32_t>(xr[c]) << 16);
+  __syncthreads();
+  for (int e = wv; e < E; e += 4) {
+    const float* we = wr + static_cast<int64_t>(e) * d;
+    float acc = 0.0f;
+#pragma unroll 8
+    for (int c = lane; c < d; c += kWave) acc = __fmaf_rn(xs[c], we[c], acc);
+    float v = tree_sum(acc);
+    if (bias) v = v + bias[e];
+    if (lane == 0) lgs[e] = v;
+  }
+  __syncthreads();
+  if (wv != 0) return;
   constexpr int kMaxPer = MOE_MAX_EXPERTS / kWave;
   float lg[kMaxPer];
 #pragma unroll
-  for (int m = 0; m < kMaxPer; m++) lg[m] = -INFINITY;
-  for (int e = 0; e < E; e++) {
-    const float* we = wr + static_cast<int64_t>(e) * d;
-    float acc = 0.0f;
-    for (int c = lane; c < d; c += kWave)
-      acc = __fmaf_rn(__uint_as_float(static_cast<uint32_t>(xr[c]) << 16), we[c], acc);
-    float v = tree_sum(acc);
-    if (bias) v = v + bias[e];
-#pragma unroll
-    for (int m = 0; m < kMaxPer; m++)
-      if (e == m * kWave + lane) lg[m] = v;
+  for (int m = 0; m < kMaxPer; m++) {
+    const int e = m * kWave + lane;
+    lg[m] = e < E ? lgs[e] : -INFINITY;
   }
   // top-k by (logit desc, index asc); every lane ends with the same picks
-  uint64_t taken[kMaxPer];
+  bool taken[kMaxPer];
   int ids[MOE_MAX_TOPK];
   float sel[MOE_MAX_TOPK];
 #pragma unroll
-  for (int m = 0; m < kMaxPer; m++) taken[m] = 0;
+  for (int m = 0; m < kMaxPer; m++) taken[m] = false;
   for (int j = 0; j < k; j++) {
     float bv = -INFINITY;
     int bi = 0x7FFFFFFF;
@@ -104,7 +116,7 @@ route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __r
     sel[j] = bv;
 #pragma unroll
     for (int m = 0; m < kMaxPer; m++)
-      if (bi == m * kWave + lane) taken[m] = 1;
+      if (bi == m * kWave + lane) taken[m] = true;
   }
   if (lane == 0) {
     float ex[MOE_MAX_TOPK];
@@ -236,7 +248,8 @@ extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const 
                                  int32_t* perm_token, int32_t* inv_perm, uint16_t* x_perm,
                                  void* ws, size_t ws_bytes, void* stream) {
   using namespace moe;
-  if (T < 0 || d <= 0 || d % 64 || E <= 0 || S < 0 || E + S > MOE_MAX_EXPERTS) return MOE_ERR_ARG;
+  if (T < 0 || d <= 0 || d % 64 || d > kMaxD || E <= 0 || S < 0 || E + S > MOE_MAX_EXPERTS)
+    return MOE_ERR_ARG;
   if (k < 1 || k > E || k > MOE_MAX_TOPK) return MOE_ERR_ARG;
   if (!offsets || (T > 0 && (!x || !w_router || !topk_ids || !topk_w || !perm_token || !inv_perm)))
     return MOE_ERR_ARG;
@@ -248,7 +261,7 @@ extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const 
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + need / 2);
   if (T > 0) {
-    hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(cdiv(T, 4))), dim3(256), 0, s,
+    hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(T)), dim3(256), 0, s,
                        x, T, d, w_router, bias, E, k, topk_ids, topk_w);
     hipLaunchKernelGGL(route_hist_kernel, dim3(n_chunks), dim3(64), 0, s, topk_ids, T, E, k, hist);
   }

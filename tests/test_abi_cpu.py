@@ -78,7 +78,7 @@ def test_route_validation(lib):
     assert call(k=9) == -1
     assert call(k=0) == -1
     assert call(k=17, E=32) == -1
-    assert call(E=500, S=20) == -1
+    assert call(E=250, S=20) == -1
     assert call(ws=None) == -4
     assert call(wsb=ws_need - 1) == -4
     assert call(xp=MISALIGNED) == -3
@@ -114,7 +114,7 @@ def _fake_layer(n_slots=4, hdr=None):
         K.copy_codes = K.copy_sz = K.copy_hdr = FAKE.value
         K.copy_hdr_host = hdr.ctypes.data
         K.row_slot = FAKE.value
-    L.order_gu = L.order_dn = L.staging = FAKE.value
+    L.order_gu = L.order_dn = L.n_base = L.staging = FAKE.value
     return L, keep
 
 
