@@ -15,13 +15,16 @@ from __future__ import annotations
 
 import argparse
 import ctypes as C
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
 import numpy as np
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 
@@ -109,18 +112,59 @@ def describe(wk):
     return d
 
 
-def cpu_baseline(wk, inputs, batch, n_tok):
+def measured_traffic(workload):
+    """HBM bytes per gate/up launch from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE passes scaled by a plain copy's reading), or
+    None when there is none for this workload or the kernel sources have
+    changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_ffn_gateup_%s.md" % workload.replace("-", "_"))
+    if not os.path.exists(path):
+        return None
+    kv = dict(re.findall(r"^(\w+): (\S+)$", open(path).read(), flags=re.M))
+    h = hashlib.sha256()
+    for f in ("ffn.hip", "common.hpp"):
+        with open(os.path.join(ROOT, "paper_2503_21135_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if kv.get("workload") != workload or kv.get("source_sha256_16") != h.hexdigest()[:16]:
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
+def cpu_baseline(wk, inputs, batch, min_seconds):
+    """The oracle on a bounded sample of the same step: routing and
+    permutation of the whole batch, then the fp64 SiLU-GLU FFN of the rows
+    routed to the busiest expert, repeated until `min_seconds` have passed.
+    That expert's dequantized matrices (the oracle's resident form of the
+    packed weights) are prepared before the clock starts, as the packed
+    weights are on the GPU side.  tokens/s counts k expert rows as one token."""
     import oracle
+    cfg = wk.layer
+    k = cfg.top_k
     rs = oracle.switch_state(inputs, epoch=0)
-    toks = np.arange(min(n_tok, wk.tokens))
+    _, ids, _ = oracle.route(batch.x, inputs.router, k, batch.bias)
+    off, perm, _ = oracle.permute(ids, cfg.n_experts, cfg.n_shared)
+    e = int(np.argmax(np.diff(off[:cfg.n_experts + 1])))
+    W = [oracle.effective_weight(inputs.weight(e, kd), int(inputs.bits[e]), cfg.group,
+                                 np.nonzero(rs[kd][e] >= 0)[0]) for kd in (0, 1, 2)]
+    rows = perm[off[e]:off[e + 1]]
+    reps = 0
     t0 = time.perf_counter()
-    oracle.layer_forward(inputs, batch.x, bias=batch.bias, row_slot=rs, tokens=toks)
-    dt = time.perf_counter() - t0
-    return {"value": round(len(toks) / dt, 4), "unit": "tokens/s", "cores": oracle.num_threads(),
+    while True:
+        _, ids, _ = oracle.route(batch.x, inputs.router, k, batch.bias)
+        oracle.permute(ids, cfg.n_experts, cfg.n_shared)
+        oracle.expert_ffn(W[0], W[1], W[2], batch.x, rows)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    tok = reps * len(rows) / k
+    return {"value": round(tok / dt, 4), "unit": "tokens/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": "%d of %d tokens of the same batch: router for all tokens, "
-                      "quantize+dequantize of every expert those tokens reach, fp64 FFN, "
-                      "combine (%.1f s)" % (len(toks), wk.tokens, dt)}
+            "sample": "%d x (route+permute of all %d tokens, fp64 FFN of the %d rows of "
+                      "expert %d at %d bits, %d%% of rows switched); %d expert rows = "
+                      "%.1f tokens at top-%d in %.1f s"
+                      % (reps, wk.tokens, len(rows), e, int(inputs.bits[e]),
+                         inputs.switch_percent(0), reps * len(rows), tok, k, dt)}
 
 
 def main():
@@ -129,7 +173,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="mixtral-decode")
-    ap.add_argument("--cpu-tokens", type=int, default=4)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="minimum CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device-to-device copies of MIB MiB (the "
@@ -230,15 +275,15 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle on %d tokens ..." % args.cpu_tokens)
-        cpu = cpu_baseline(wk, inputs, batch, args.cpu_tokens)
+        log("timing the CPU oracle for at least %.0f s ..." % args.cpu_seconds)
+        cpu = cpu_baseline(wk, inputs, batch, args.cpu_seconds)
         log("cpu baseline", cpu)
 
     bound = "hbm"
     roof = {"bound": bound, "kernel": "ffn_stream_kernel<NK=2> (gate+up expert projections, "
                                       "SiLU-GLU epilogue)",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.workload),
             "algorithmic_bytes_per_launch": int(byt["gate_up"]),
             "avg_launch_ms": round(gu_ms, 5)}
     out = {
