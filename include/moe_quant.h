@@ -138,9 +138,11 @@ typedef struct moe_kind_desc {
  *
  * order_gu[e*d_ff + i] and order_dn[e*d_model + i] (routed experts only) are
  * the orders in which the FFN visits hidden neurons and output channels.  They
- * are rebuilt by moe_set_channel_switch as stable partitions: first the rows
- * whose sources are all base codes (n_base[e] of them for gate/up neurons,
- * n_base[E + e] for down channels), then the rows reading a cached copy.
+ * are rebuilt by moe_set_channel_switch as stable partitions by source class:
+ * for a hidden neuron, class bit 0 = its gate row reads a cached copy, bit 1 =
+ * its up row does; for an output channel, class 1 = its down row does.  Rows
+ * of class 0 come first (ascending), then class 1, 2, 3.  class_cnt[e*4 + c]
+ * (gate/up) and class_cnt[4*E + e*4 + c] (down) count the rows of each class.
  * Any permutation gives the same result.
  */
 typedef struct moe_layer {
@@ -155,7 +157,7 @@ typedef struct moe_layer {
   moe_kind_desc_t kind[3];
   int32_t* order_gu;          /* device [E][d_ff]    */
   int32_t* order_dn;          /* device [E][d_model] */
-  int32_t* n_base;            /* device [2][E]: leading base-only rows of the orders */
+  int32_t* class_cnt;         /* device [2][E][4]: rows per source class of the orders */
   int32_t* staging;           /* device scratch of at least max(kind[].n_slots)+1 int32 */
 } moe_layer_t;
 
@@ -289,8 +291,8 @@ int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
  *   kind      MOE_KIND_GATE/UP/DOWN, or -1 with n_on == 0 to reset all kinds.
  *   slots_on  host int32 list of n_on distinct slots in [0, n_slots) whose
  *             headers name distinct rows; copied before the call returns.
- *   Rewrites kind[kind].row_slot, order_gu and n_base[0..E) (gate/up) or
- *   order_dn and n_base[E..2E) (down).
+ *   Rewrites kind[kind].row_slot, order_gu and class_cnt[0..4E) (gate/up) or
+ *   order_dn and class_cnt[4E..8E) (down).
  */
 int moe_set_channel_switch(moe_layer_t* L, int32_t kind,
                            const int32_t* slots_on, int32_t n_on, void* stream);

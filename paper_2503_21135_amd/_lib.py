@@ -39,7 +39,7 @@ class LayerDesc(C.Structure):
         ("n_experts", C.c_int32), ("n_shared", C.c_int32), ("d_model", C.c_int32),
         ("d_ff", C.c_int32), ("d_ff_shared", C.c_int32), ("group", C.c_int32),
         ("bits_host", C.c_void_p), ("bits", C.c_void_p), ("kind", KindDesc * 3),
-        ("order_gu", C.c_void_p), ("order_dn", C.c_void_p), ("n_base", C.c_void_p),
+        ("order_gu", C.c_void_p), ("order_dn", C.c_void_p), ("class_cnt", C.c_void_p),
         ("staging", C.c_void_p),
     ]
 

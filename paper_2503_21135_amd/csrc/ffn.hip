@@ -31,13 +31,14 @@
 //     tokens 4*kq .. 4*kq+3, so the lane applies its own row's scale/zero.
 #include <algorithm>
 #include <type_traits>
+#include <vector>
 
 #include "common.hpp"
 
 namespace moe {
 namespace {
 
-constexpr int kRowsPerWG = 128;          // rows of one kind per workgroup (64 at NT = 4)
+constexpr int kRowsPerWG = 128;          // row counts must be multiples of this
 constexpr uint32_t kMagic = 0x43004300u;  // two bf16 128.0
 
 struct KindDev {
@@ -55,7 +56,7 @@ struct FfnArgs {
   const int32_t* bits;
   const int32_t* order_gu;
   const int32_t* order_dn;
-  const int32_t* n_base;
+  const int32_t* class_cnt;
   const uint16_t* x;
   const float* xsum;   // [d/g][rows] group sums of the gathered x rows
   const int32_t* offsets;
@@ -64,14 +65,11 @@ struct FfnArgs {
   float* hsum;         // [max(f,fs)/g][rows] group sums of h rows
   float* o;
   int64_t split_stride;
+  uint32_t x_bytes, h_bytes, xsum_bytes, hsum_bytes;   // resource sizes (< 2^31)
+  uint32_t copy_bytes[3], copy_sz_bytes[3];
   int E, S, d, f, fs, group;
   int Tk;    // routed rows T*k
   int rows;  // all permuted rows T*(k+S)
-};
-
-// Experts in the order their waves are launched (most bytes first).
-struct Sched {
-  int16_t e[MOE_MAX_EXPERTS];
 };
 
 // Row-offset of permuted row p in the h buffer (routed rows have d_ff
@@ -79,74 +77,6 @@ struct Sched {
 __device__ __forceinline__ int64_t h_row(const FfnArgs& a, int p) {
   return p < a.Tk ? static_cast<int64_t>(p) * a.f
                   : static_cast<int64_t>(a.Tk) * a.f + static_cast<int64_t>(p - a.Tk) * a.fs;
-}
-
-// Where one row's codes and {scale, zero} words live.
-struct RowSrc {
-  const uint32_t* row;  // first code word of the row
-  const uint32_t* sz;   // {s16, z} word of group 0
-  int sz_stride;        // words between consecutive groups
-  int bits;
-};
-
-__device__ __forceinline__ RowSrc row_source(const KindDev& k, int e, bool routed, int R, int K,
-                                             int bits_e, int row, int group) {
-  RowSrc r;
-  const int slot = routed ? k.row_slot[static_cast<int64_t>(e) * R + row] : -1;
-  if (slot < 0) {
-    r.row = k.codes + k.code_off[e] + static_cast<int64_t>(row) * (K * bits_e / 32);
-    r.sz = k.sz + k.sz_off[e] + row;
-    r.sz_stride = R;
-    r.bits = bits_e;
-  } else {
-    r.row = k.copy_codes + static_cast<int64_t>(slot) * (K / 4);
-    r.sz = k.copy_sz + static_cast<int64_t>(slot) * (K / group);
-    r.sz_stride = 1;
-    r.bits = 8;
-  }
-  return r;
-}
-
-// Load `nw` code words (nw in {1,2,3,4,8}) of this lane's share of a group.
-template <int NW>
-__device__ __forceinline__ void load_words(uint32_t (&cw)[NW], const uint32_t* p) {
-  if constexpr (NW == 8) {
-    const u32x4 a = reinterpret_cast<const u32x4*>(p)[0];
-    const u32x4 b = reinterpret_cast<const u32x4*>(p)[1];
-    cw[0] = a[0]; cw[1] = a[1]; cw[2] = a[2]; cw[3] = a[3];
-    cw[4] = b[0]; cw[5] = b[1]; cw[6] = b[2]; cw[7] = b[3];
-  } else if constexpr (NW == 4) {
-    const u32x4 a = reinterpret_cast<const u32x4*>(p)[0];
-    cw[0] = a[0]; cw[1] = a[1]; cw[2] = a[2]; cw[3] = a[3];
-  } else if constexpr (NW == 2) {
-    const u32x2 a = reinterpret_cast<const u32x2*>(p)[0];
-    cw[0] = a[0]; cw[1] = a[1];
-  } else {
-#pragma unroll
-    for (int i = 0; i < NW; i++) cw[i] = p[i];
-  }
-}
-
-__device__ __forceinline__ void load_chunk(uint32_t (&cw)[8], const uint32_t* p, int nw) {
-  if (nw == 8) {
-    uint32_t t[8];
-    load_words<8>(t, p);
-#pragma unroll
-    for (int i = 0; i < 8; i++) cw[i] = t[i];
-  } else if (nw == 4) {
-    uint32_t t[4];
-    load_words<4>(t, p);
-#pragma unroll
-    for (int i = 0; i < 4; i++) cw[i] = t[i];
-  } else if (nw == 3) {
-    cw[0] = p[0]; cw[1] = p[1]; cw[2] = p[2];
-  } else if (nw == 2) {
-    uint32_t t[2];
-    load_words<2>(t, p);
-    cw[0] = t[0]; cw[1] = t[1];
-  } else {
-    cw[0] = p[0];
-  }
 }
 
 __device__ __forceinline__ uint32_t pair8(uint32_t w, int hi) {
@@ -195,121 +125,128 @@ __device__ __forceinline__ void dequant_b(const uint32_t (&cw)[NW], u32x4 (&wf)[
   }
 }
 
-template <int NM>
-__device__ __forceinline__ void dequant_rt(const uint32_t (&cw)[8], int bits, u32x4 (&wf)[NM]) {
-  if (bits == 4) {
-    uint32_t t[NM];
-#pragma unroll
-    for (int i = 0; i < NM; i++) t[i] = cw[i];
-    dequant_b<4, NM, NM>(t, wf);
-  } else if (bits == 2) {
-    uint32_t t[NM / 2];
-#pragma unroll
-    for (int i = 0; i < NM / 2; i++) t[i] = cw[i];
-    dequant_b<2, NM, NM / 2>(t, wf);
-  } else if (bits == 8) {
-    uint32_t t[2 * NM];
-#pragma unroll
-    for (int i = 0; i < 2 * NM; i++) t[i] = cw[i];
-    dequant_b<8, NM, 2 * NM>(t, wf);
-  } else {
-    if constexpr (NM == 4) {
-      uint32_t t[3] = {cw[0], cw[1], cw[2]};
-      dequant_b<3, NM, 3>(t, wf);
-    }
-  }
-}
-
 __device__ __forceinline__ float silu_mul(float g, float u) {
   return g / (1.0f + __expf(-g)) * u;
 }
 
-// ------------------------------------------------------------------ streaming kernel
-// One workgroup = 4 waves on one expert.  Each wave owns 16*RT consecutive
-// positions of the expert's row order for each of NK weight kinds (NK = 2:
-// the gate and up rows of the same neurons; NK = 1: down rows = output
-// channels) and streams their packed codes through registers; the
-// activations of the workgroup's token tile (NT*16 rows) are staged in LDS
-// two groups at a time (double-buffered, one barrier per chunk), so every
-// wave reads them from LDS rather than L2.  The codes of the next group are
-// in flight while the current group is dequantized and contracted.
-//
-// Two passes cover an expert's rows: the base pass takes the leading rows of
-// the order whose sources are all base codes (bit-width B of the expert, code
-// registers sized for B); the switched pass takes the rest, each lane reading
-// its own source (base codes or an 8-bit copy) at its own width.
+// ------------------------------------------------------------------ buffer loads
+// Every load of the streaming loop is a raw buffer load through a
+// range-checked resource.  A lane whose offset lies past the resource reads
+// zeros without touching memory, so dead rows, groups past the end of a K
+// slice and padding tokens need no branch around their loads: the loop stays
+// straight-line and the compiler's wait counts keep every prefetch stage in
+// flight (a branch around a load makes it drain all outstanding loads).
+constexpr uint32_t kOOB = 0x80000000u;   // past every resource: sizes are < 2^31
 
-constexpr int kWaves = 4;
+typedef __amdgpu_buffer_rsrc_t Rsrc;
 
-// Workgroups [first[i], first[i+1]) of a launch serve expert e[i].
-// Entry i is expert e[i] in the switched pass when sw[i] != 0, in the base
-// pass otherwise.
-struct WgMap {
-  int n;
-  int32_t first[2 * MOE_MAX_EXPERTS + 1];
-  int16_t e[2 * MOE_MAX_EXPERTS];
-  int8_t sw[2 * MOE_MAX_EXPERTS];
-};
-
-__device__ __forceinline__ int map_find(const WgMap& m, int wg) {
-  int lo = 0, hi = m.n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (m.first[mid] <= wg) lo = mid; else hi = mid - 1;
-  }
-  return lo;
+__device__ __forceinline__ Rsrc make_rsrc(const void* p, uint32_t bytes) {
+  // word 3 = 0x00020000: 32-bit data format, raw (unswizzled) addressing
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
 }
 
-// B > 0: all rows read B-bit codes.  B == 0: per-lane width (<= 8 words).
-template <int NM, int B>
-struct CodeWords {
-  static constexpr int value = B == 0 ? 8 : NM * B / 4;
-};
+__device__ __forceinline__ u32x4 bload4(Rsrc r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
 
-template <int NM, int RT, int NK, int B>
-struct CodeStage {
-  uint32_t cw[RT][NK][CodeWords<NM, B>::value];
-  uint32_t szw[RT][NK];
-};
-
-// Where the rows of one kind live for a wave.  B > 0: every row reads its
-// expert's base codes, so the bases are wave-uniform and each lane keeps
-// 32-bit offsets; B == 0: each lane keeps its own full source.
-template <int RT, int NK, int B>
-struct Rows {
-  const uint32_t* cbase[NK];   // B > 0: codes of the expert
-  const uint32_t* sbase[NK];   // B > 0: {scale, zero} words of the expert
-  uint32_t coff[RT][NK];       // B > 0: word offset of the lane's row
-  uint32_t soff[RT][NK];       // B > 0: offset of the lane's row, group 0
-  int sstride;                 // B > 0: rows of the expert (group stride)
-  RowSrc src[B == 0 ? RT : 1][B == 0 ? NK : 1];  // B == 0
-};
-
-template <int NM, int RT, int NK, int B>
-__device__ __forceinline__ void load_stage(CodeStage<NM, RT, NK, B>& st, const Rows<RT, NK, B>& rw,
-                                           const bool (&live)[RT], int gi, int kq) {
-  constexpr int g = NM * 32;
-  constexpr int NW = CodeWords<NM, B>::value;
+template <int NW>
+__device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off) {
+  if constexpr (NW == 8) {
+    const u32x4 a = bload4(r, off);
+    const u32x4 b = bload4(r, off + 16u);
 #pragma unroll
-  for (int rt = 0; rt < RT; rt++)
-#pragma unroll
-    for (int kk = 0; kk < NK; kk++) {
-      if (!live[rt]) {
-#pragma unroll
-        for (int w = 0; w < NW; w++) st.cw[rt][kk][w] = 0u;
-        st.szw[rt][kk] = 0u;
-        continue;
-      }
-      if constexpr (B == 0) {
-        const RowSrc& s = rw.src[rt][kk];
-        const int nw = g * s.bits / 128;
-        load_chunk(st.cw[rt][kk], s.row + gi * (g * s.bits / 32) + kq * nw, nw);
-        st.szw[rt][kk] = s.sz[static_cast<int64_t>(gi) * s.sz_stride];
-      } else {
-        load_words<NW>(st.cw[rt][kk], rw.cbase[kk] + rw.coff[rt][kk] + gi * (g * B / 32) + kq * NW);
-        st.szw[rt][kk] = rw.sbase[kk][rw.soff[rt][kk] + static_cast<uint32_t>(gi) * rw.sstride];
-      }
+    for (int i = 0; i < 4; i++) {
+      cw[i] = a[i];
+      cw[4 + i] = b[i];
     }
+  } else if constexpr (NW == 4) {
+    const u32x4 a = bload4(r, off);
+#pragma unroll
+    for (int i = 0; i < 4; i++) cw[i] = a[i];
+  } else if constexpr (NW == 3) {
+    const auto a = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, 0);
+    cw[0] = a[0]; cw[1] = a[1]; cw[2] = a[2];
+  } else if constexpr (NW == 2) {
+    const auto a = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    cw[0] = a[0]; cw[1] = a[1];
+  } else {
+    cw[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+  }
+}
+
+// ------------------------------------------------------------------ streaming kernel
+// One workgroup = 4 waves on one expert and one source class of its rows.
+// Each wave owns 16*RT consecutive positions of the expert's row order for
+// each of NK weight kinds (NK = 2: the gate and up rows of the same neurons;
+// NK = 1: down rows = output channels).  Within a class every kind has one
+// source for all rows -- the expert's base codes at bit-width B, or the
+// cached 8-bit copies -- so the loads are wave-uniform in shape and the code
+// registers are sized for that width (template BG / BU).  The packed codes of
+// the next kStages groups are in flight in registers while the current group
+// is dequantized and contracted; the activations of the workgroup's token
+// tile (NT*16 rows) are staged in LDS two groups at a time (double-buffered,
+// one barrier per two groups), so every wave reads them from LDS.
+
+constexpr int kWaves = 4;
+constexpr int kStages = 4;   // groups of codes in flight per wave
+
+// Work of one launch over experts e0 .. e0+n_e-1.  Every workgroup covers
+// kWaves*16 row positions of one source class of one expert.  Workgroups
+// [0, n_e*n_sw) take the switched classes (n_sw per expert, an upper bound
+// on what its copies can need; those beyond the expert's actual class sizes
+// exit at once); the rest take class 0, per_e workgroups per expert, experts
+// in the order `order` (widest bit-width first).
+struct WgMap {
+  int e0, n_e;
+  int n_sw;
+  int per_e;
+  int16_t order[MOE_MAX_EXPERTS];
+};
+
+template <int NM, int B>
+constexpr int kWords = NM * B / 4;   // code words per lane per group
+
+template <int NM, int RT, int BG, int BU>
+struct Stage {
+  uint32_t cg[RT][(kWords<NM, BG>)];
+  uint32_t cu[RT][(kWords<NM, BU>)];   // unused for NK = 1
+  uint32_t szw[RT][2];
+};
+
+// Source of one kind for a workgroup: resources, per-group strides and the
+// lane's byte offsets (kOOB for lanes past the rows of the class).
+template <int RT>
+struct Src {
+  Rsrc code, sz;
+  uint32_t sz_gstride;     // bytes between consecutive groups' {s, z} words
+  uint32_t coff[RT];       // byte offset of the lane's code share of group 0
+  uint32_t soff[RT];       // byte offset of the row's {s, z} word of group 0
+};
+
+template <int NM, int B, int RT>
+__device__ __forceinline__ void load_kind(uint32_t (&cw)[RT][(kWords<NM, B>)], uint32_t (&szw)[RT],
+                                          const Src<RT>& s, int gi, bool gv) {
+  constexpr uint32_t gcb = NM * 32 * B / 8;   // code bytes per row and group
+#pragma unroll
+  for (int rt = 0; rt < RT; rt++) {
+    bload<kWords<NM, B>>(cw[rt], s.code, gv ? s.coff[rt] + gi * gcb : kOOB);
+    szw[rt] = __builtin_amdgcn_raw_buffer_load_b32(s.sz, gv ? s.soff[rt] + gi * s.sz_gstride : kOOB,
+                                                   0, 0);
+  }
+}
+
+template <int NM, int RT, int NK, int BG, int BU>
+__device__ __forceinline__ void load_stage(Stage<NM, RT, BG, BU>& st, const Src<RT> (&src)[2], int gi,
+                                           bool gv) {
+  uint32_t s0[RT], s1[RT];
+  load_kind<NM, BG, RT>(st.cg, s0, src[0], gi, gv);
+  if constexpr (NK == 2) load_kind<NM, BU, RT>(st.cu, s1, src[1], gi, gv);
+#pragma unroll
+  for (int rt = 0; rt < RT; rt++) {
+    st.szw[rt][0] = s0[rt];
+    if constexpr (NK == 2) st.szw[rt][1] = s1[rt];
+  }
 }
 
 // Contract one group: A fragments (activations) come from LDS.
@@ -321,9 +258,8 @@ __device__ __forceinline__ void load_stage(CodeStage<NM, RT, NK, B>& st, const R
 // wait-state insertion was observed to fall short (the last accumulator
 // element was read stale).  The 3 x s_nop 7 (24 wait states) cover the
 // longest 16x16x32 bf16 MFMA latency on gfx950.
-template <int NM, int NT, int RT, int NK, int B>
-__device__ __forceinline__ void compute_group(const CodeStage<NM, RT, NK, B>& st,
-                                              const Rows<RT, NK, B>& rw,
+template <int NM, int NT, int RT, int NK, int BG, int BU>
+__device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st,
                                               const u32x4 (&af)[NT][NM], const f32x4 (&X)[NT],
                                               f32x4 (&acc)[RT][NK][NT]) {
   f32x4 tmp[RT][NK][NT];
@@ -333,14 +269,14 @@ __device__ __forceinline__ void compute_group(const CodeStage<NM, RT, NK, B>& st
 #pragma unroll
     for (int kk = 0; kk < NK; kk++) {
       u32x4 wf[NM];
+      constexpr int Bk0 = BG, Bk1 = BU;
       float off;
-      if constexpr (B == 0) {
-        const int bits = rw.src[rt][kk].bits;
-        dequant_rt<NM>(st.cw[rt][kk], bits, wf);
-        off = bits == 8 ? 0.f : 128.f;
+      if (kk == 0) {
+        dequant_b<Bk0, NM, kWords<NM, Bk0>>(st.cg[rt], wf);
+        off = Bk0 == 8 ? 0.f : 128.f;
       } else {
-        dequant_b<B, NM, CodeWords<NM, B>::value>(st.cw[rt][kk], wf);
-        off = B == 8 ? 0.f : 128.f;
+        dequant_b<Bk1, NM, kWords<NM, Bk1>>(st.cu[rt], wf);
+        off = Bk1 == 8 ? 0.f : 128.f;
       }
       sc[rt][kk] = fp16_bits_to_f32(st.szw[rt][kk] & 0xFFFFu);
       zz[rt][kk] = fp16_bits_to_f32(st.szw[rt][kk] >> 16) + off;
@@ -377,10 +313,11 @@ struct XTile {
   float xs[2][2][TOK];
 };
 
-// The expert's rows at order positions [pos0, pos1) (lanes past pos1 idle),
-// token tile passes over the expert's segment, K groups [g0, g1) of split sp.
-template <int NM, int NT, int RT, int NK, int B>
-__device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0, int pos1,
+// The rows at order positions [pos0, pos1) of expert e (lanes past pos1
+// idle), class cls (bit kk set: kind kk reads the 8-bit copies), token tile
+// passes over the expert's segment, K groups [g0, g1) of split sp.
+template <int NM, int NT, int RT, int NK, int BG, int BU>
+__device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int cls, int pos0, int pos1,
                             int R, int sp, int n_split) {
   constexpr int g = NM * 32;
   constexpr int KC = XTile<NM, NT>::KC;
@@ -388,6 +325,7 @@ __device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0
   constexpr int PIECES = TOK * KC / 8;   // 16-byte pieces per chunk
   constexpr int PPT = PIECES / 256;
   static_assert(PIECES % 256 == 0, "chunk must split evenly over the workgroup");
+  static_assert(kStages == 4, "the loop body below handles four groups");
   const int tid = threadIdx.x;
   const int wv = tid >> 6;
   const int lane = tid & 63;
@@ -402,66 +340,77 @@ __device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0
   const int g0 = sp * G / n_split;
   const int g1 = (sp + 1) * G / n_split;
   const int be = a.bits[e];
-  const KindDev* kinds = down ? &a.kd[2] : &a.kd[0];
+  const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
-  const float* xsum = down ? a.hsum : a.xsum;
 
   int row_id[RT];
   bool live[RT];
-  Rows<RT, NK, B> rw;
-  rw.sstride = R;
-#pragma unroll
-  for (int kk = 0; kk < NK; kk++) {
-    rw.cbase[kk] = kinds[kk].codes + kinds[kk].code_off[e];
-    rw.sbase[kk] = kinds[kk].sz + kinds[kk].sz_off[e];
-  }
 #pragma unroll
   for (int rt = 0; rt < RT; rt++) {
     const int pos = pos0 + wv * 16 * RT + rt * 16 + r16;
     live[rt] = pos < pos1;
     row_id[rt] = live[rt] ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+  }
+  Src<RT> src[2];
 #pragma unroll
-    for (int kk = 0; kk < NK; kk++) {
-      if constexpr (B == 0) {
-        rw.src[rt][kk] = row_source(kinds[kk], e, routed, R, K, be, row_id[rt], g);
-      } else {
-        rw.coff[rt][kk] = static_cast<uint32_t>(row_id[rt]) * static_cast<uint32_t>(K * B / 32);
-        rw.soff[rt][kk] = static_cast<uint32_t>(row_id[rt]);
+  for (int kk = 0; kk < NK; kk++) {
+    const KindDev& kd = a.kd[kind0 + kk];
+    const bool copy = (cls >> kk) & 1;
+    Src<RT>& s = src[kk];
+    if (!copy) {
+      const uint32_t row_bytes = static_cast<uint32_t>(K) * be / 8;
+      const uint32_t words = static_cast<uint32_t>(g) * be / 128;   // per lane per group
+      s.code = make_rsrc(kd.codes + kd.code_off[e], static_cast<uint32_t>(R) * row_bytes);
+      s.sz = make_rsrc(kd.sz + kd.sz_off[e], static_cast<uint32_t>(R) * G * 4u);
+      s.sz_gstride = static_cast<uint32_t>(R) * 4u;
+#pragma unroll
+      for (int rt = 0; rt < RT; rt++) {
+        s.coff[rt] = live[rt] ? row_id[rt] * row_bytes + kq * words * 4u : kOOB;
+        s.soff[rt] = live[rt] ? row_id[rt] * 4u : kOOB;
+      }
+    } else {
+      s.code = make_rsrc(kd.copy_codes, a.copy_bytes[kind0 + kk]);
+      s.sz = make_rsrc(kd.copy_sz, a.copy_sz_bytes[kind0 + kk]);
+      s.sz_gstride = 4u;
+#pragma unroll
+      for (int rt = 0; rt < RT; rt++) {
+        const int slot = live[rt] ? kd.row_slot[static_cast<int64_t>(e) * R + row_id[rt]] : -1;
+        s.coff[rt] = slot >= 0 ? static_cast<uint32_t>(slot) * K + kq * (g / 4) : kOOB;
+        s.soff[rt] = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
       }
     }
   }
+  const float* xsum = down ? a.hsum : a.xsum;
+  const Rsrc xr = make_rsrc(down ? a.h : a.x, down ? a.h_bytes : a.x_bytes);
+  const Rsrc xsr = make_rsrc(xsum, down ? a.hsum_bytes : a.xsum_bytes);
 
   for (int t0 = seg0; t0 < seg1; t0 += TOK) {
     // piece q = tid + 256*i of a chunk: token row q / (KC/8), column (q % (KC/8))*8
-    uint32_t arow[PPT];   // element offset of the row, 0xFFFFFFFF when absent
+    uint32_t arow[PPT];   // byte offset of the token's row, kOOB when absent
 #pragma unroll
     for (int i = 0; i < PPT; i++) {
       const int p = t0 + (tid + 256 * i) / (KC / 8);
-      arow[i] = p < seg1 ? static_cast<uint32_t>(down ? h_row(a, p)
-                                                      : static_cast<int64_t>(a.perm[p]) * K)
-                         : 0xFFFFFFFFu;
+      arow[i] = p < seg1 ? static_cast<uint32_t>(2 * (down ? h_row(a, p)
+                                                          : static_cast<int64_t>(a.perm[p]) * K))
+                         : kOOB;
     }
-    const uint16_t* abase = down ? a.h : a.x;
     const int acol = (tid % (KC / 8)) * 8;   // same column for every piece of a thread
+    const int xs_g = tid / TOK, xs_j = tid % TOK;   // xsum entry of threads < 2*TOK
+    const bool xs_live = tid < 2 * TOK && t0 + xs_j < seg1;
     auto stage_x = [&](u32x4 (&v)[PPT], float& xsv, int gc) {
       const bool in_k = gc + acol / g < g1;   // the chunk's second group may not exist
 #pragma unroll
       for (int i = 0; i < PPT; i++)
-        v[i] = (arow[i] != 0xFFFFFFFFu && in_k)
-                   ? *reinterpret_cast<const u32x4*>(abase + arow[i] + gc * g + acol)
-                   : u32x4{0u, 0u, 0u, 0u};
-      xsv = 0.f;
-      if (tid < 2 * TOK) {
-        const int gg = tid / TOK, j = tid % TOK;
-        if (gc + gg < g1 && t0 + j < seg1)
-          xsv = xsum[static_cast<int64_t>(gc + gg) * a.rows + t0 + j];
-      }
+        v[i] = bload4(xr, (in_k && arow[i] != kOOB) ? arow[i] + 2u * (gc * g + acol) : kOOB);
+      const bool ok = xs_live && gc + xs_g < g1;
+      xsv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+          xsr, ok ? 4u * static_cast<uint32_t>((gc + xs_g) * a.rows + t0 + xs_j) : kOOB, 0, 0));
     };
     auto write_x = [&](const u32x4 (&v)[PPT], float xsv, int buf) {
 #pragma unroll
       for (int i = 0; i < PPT; i++)
         *reinterpret_cast<u32x4*>(&tl.x[buf][(tid + 256 * i) / (KC / 8)][acol]) = v[i];
-      if (tid < 2 * TOK) tl.xs[buf][tid / TOK][tid % TOK] = xsv;
+      if (tid < 2 * TOK) tl.xs[buf][xs_g][xs_j] = xsv;
     };
 
     f32x4 acc[RT][NK][NT];
@@ -472,9 +421,9 @@ __device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0
 #pragma unroll
         for (int nt = 0; nt < NT; nt++) acc[rt][kk][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    CodeStage<NM, RT, NK, B> s0, s1;
-    load_stage(s0, rw, live, g0, kq);
-    if (g0 + 1 < g1) load_stage(s1, rw, live, g0 + 1, kq);
+    Stage<NM, RT, BG, BU> st[kStages];
+#pragma unroll
+    for (int s = 0; s < kStages; s++) load_stage<NM, RT, NK, BG, BU>(st[s], src, g0 + s, g0 + s < g1);
     {
       u32x4 v[PPT];
       float xsv;
@@ -482,15 +431,8 @@ __device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0
       write_x(v, xsv, 0);
     }
     __syncthreads();
-    int buf = 0;
-    for (int gc = g0; gc < g1; gc += 2) {
-      const bool more = gc + 2 < g1;
-      u32x4 vn[PPT];
-      float xsn = 0.f;
-      if (more) stage_x(vn, xsn, gc + 2);
-#pragma unroll
-      for (int gg = 0; gg < 2; gg++) {
-        if (gc + gg >= g1) break;
+    auto group = [&](Stage<NM, RT, BG, BU>& s, int buf, int gg, int gi) {
+      if (gi < g1) {   // wave-uniform; the loads below are unconditional
         u32x4 af[NT][NM];
         f32x4 X[NT];
 #pragma unroll
@@ -501,17 +443,23 @@ __device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0
                 &tl.x[buf][nt * 16 + r16][gg * g + kq * (g / 4) + 8 * m]);
           X[nt] = *reinterpret_cast<const f32x4*>(&tl.xs[buf][gg][nt * 16 + 4 * kq]);
         }
-        if (gg == 0) {
-          compute_group<NM, NT, RT, NK, B>(s0, rw, af, X, acc);
-          if (gc + 2 < g1) load_stage(s0, rw, live, gc + 2, kq);
-        } else {
-          compute_group<NM, NT, RT, NK, B>(s1, rw, af, X, acc);
-          if (gc + 3 < g1) load_stage(s1, rw, live, gc + 3, kq);
-        }
+        compute_group<NM, NT, RT, NK, BG, BU>(s, af, X, acc);
       }
-      if (more) write_x(vn, xsn, buf ^ 1);
+      load_stage<NM, RT, NK, BG, BU>(s, src, gi + kStages, gi + kStages < g1);
+    };
+    for (int gc = g0; gc < g1; gc += 4) {
+      u32x4 vn[PPT];
+      float xsn;
+      stage_x(vn, xsn, gc + 2);
+      group(st[0], 0, 0, gc);
+      group(st[1], 0, 1, gc + 1);
+      write_x(vn, xsn, 1);
       __syncthreads();
-      buf ^= 1;
+      stage_x(vn, xsn, gc + 4);
+      group(st[2], 1, 0, gc + 2);
+      group(st[3], 1, 1, gc + 3);
+      write_x(vn, xsn, 0);
+      __syncthreads();
     }
 
     if constexpr (NK == 2) {
@@ -543,47 +491,73 @@ __device__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int pos0
   }
 }
 
-// Rows per workgroup of the base pass for an expert of bit-width B.
-__host__ __device__ constexpr int base_rt(int B, int NT) { return (B == 8 || NT == 4) ? 1 : 2; }
 
-// One launch serves both passes of a set of experts: the switched-pass
-// workgroups come first in the grid (few, long, latency-bound), the base-pass
-// workgroups fill the machine behind them.
+template <int NM, int NT, int NK, int B>
+__device__ __forceinline__ void dispatch_class(const FfnArgs& a, XTile<NM, NT>& tl, int e, int cls,
+                                               int pos0, int pos1, int R, int sp, int n_split) {
+  if constexpr (NK == 1) {
+    if (cls == 0) stream_body<NM, NT, 1, 1, B, B>(a, tl, e, 0, pos0, pos1, R, sp, n_split);
+    else stream_body<NM, NT, 1, 1, 8, 8>(a, tl, e, 1, pos0, pos1, R, sp, n_split);
+  } else {
+    if (cls == 0) stream_body<NM, NT, 1, 2, B, B>(a, tl, e, 0, pos0, pos1, R, sp, n_split);
+    else if (cls == 1) stream_body<NM, NT, 1, 2, 8, B>(a, tl, e, 1, pos0, pos1, R, sp, n_split);
+    else if (cls == 2) stream_body<NM, NT, 1, 2, B, 8>(a, tl, e, 2, pos0, pos1, R, sp, n_split);
+    else stream_body<NM, NT, 1, 2, 8, 8>(a, tl, e, 3, pos0, pos1, R, sp, n_split);
+  }
+}
+
+// One launch serves every class of a set of experts: the switched-class
+// workgroups come first in the grid, then the class-0 workgroups, widest
+// bit-width first.
 template <int NM, int NT, int NK>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
   __shared__ __attribute__((aligned(16))) XTile<NM, NT> tl;
+  constexpr int rows = kWaves * 16;
   const int wgi = blockIdx.x / n_split;
   const int sp = blockIdx.x % n_split;
-  const int i = map_find(map, wgi);
-  const int e = map.e[i];
-  const int blk = wgi - map.first[i];
+  const int n_swg = map.n_e * map.n_sw;
+  int e, cls, blk;
+  if (wgi < n_swg) {
+    e = map.e0 + wgi / map.n_sw;
+    blk = wgi % map.n_sw;
+    cls = 0;
+  } else {
+    const int j = wgi - n_swg;
+    e = map.e0 + map.order[j / map.per_e];
+    blk = j % map.per_e;
+    cls = 0;
+  }
   if (a.offsets[e + 1] <= a.offsets[e]) return;
   const bool routed = e < a.E;
   const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
-  const int nb = routed ? a.n_base[(NK == 1 ? a.E : 0) + e] : R;
-  if (map.sw[i]) {
-    // rows past n_base: per-lane sources, 64 positions per workgroup
-    const int pos0 = nb + blk * kWaves * 16;
-    if (pos0 >= R) return;
-    const int pos1 = min(pos0 + kWaves * 16, R);
-    stream_body<NM, NT, 1, NK, 0>(a, tl, e, pos0, pos1, R, sp, n_split);
-    return;
+  int start = 0, count = R;
+  if (routed) {
+    const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+    if (wgi < n_swg) {   // find the switched class of this workgroup
+      start = cc[0];
+      cls = 4;
+      for (int c = 1; c < (NK == 1 ? 2 : 4); c++) {
+        const int nwg = (cc[c] + rows - 1) / rows;
+        if (blk < nwg) {
+          cls = c;
+          break;
+        }
+        blk -= nwg;
+        start += cc[c];
+      }
+      if (cls == 4) return;
+    }
+    count = cc[cls];
   }
+  const int pos0 = start + blk * rows;
+  if (blk * rows >= count) return;
+  const int pos1 = min(pos0 + rows, start + count);
   const int B = a.bits[e];
-  const int rows = kWaves * 16 * base_rt(B, NT);
-  const int pos0 = blk * rows;
-  if (pos0 >= nb) return;
-  const int pos1 = min(pos0 + rows, nb);
-  if (B == 8) {
-    stream_body<NM, NT, base_rt(8, NT), NK, 8>(a, tl, e, pos0, pos1, R, sp, n_split);
-  } else if (B == 4) {
-    stream_body<NM, NT, base_rt(4, NT), NK, 4>(a, tl, e, pos0, pos1, R, sp, n_split);
-  } else if (B == 2) {
-    stream_body<NM, NT, base_rt(2, NT), NK, 2>(a, tl, e, pos0, pos1, R, sp, n_split);
-  } else {
-    if constexpr (NM == 4) stream_body<NM, NT, base_rt(3, NT), NK, 3>(a, tl, e, pos0, pos1, R, sp, n_split);
-  }
+  if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
+  else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
+  else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
+  else if constexpr (NM == 4) dispatch_class<NM, NT, NK, 3>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
 }
 
 // ------------------------------------------------------------------ group sums
@@ -670,7 +644,11 @@ int validate_layer(const moe_layer_t* L) {
   if (S > 0 && (L->d_ff_shared <= 0 || L->d_ff_shared % L->group ||
                 L->d_ff_shared % kRowsPerWG))
     return MOE_ERR_ARG;
-  if (!L->bits || !L->bits_host || !L->order_gu || !L->order_dn || !L->n_base) return MOE_ERR_ARG;
+  if (!L->bits || !L->bits_host || !L->order_gu || !L->order_dn || !L->class_cnt) return MOE_ERR_ARG;
+  // buffer resources address each expert's codes and {scale, zero} words with
+  // 32-bit byte offsets below 2^31
+  const int64_t fm = std::max<int64_t>(L->d_ff, S > 0 ? L->d_ff_shared : 0);
+  if (fm * L->d_model >= (int64_t{1} << 31) / 4) return MOE_ERR_ARG;
   for (int e = 0; e < E + S; e++) {
     if (!valid_bits(L->bits_host[e])) return MOE_ERR_BITS;
     if (L->bits_host[e] == 3 && L->group != 128) return MOE_ERR_ARG;
@@ -691,47 +669,48 @@ int validate_layer(const moe_layer_t* L) {
   return MOE_OK;
 }
 
-// Work map of one launch.  Switched pass (routed experts only): enough
-// 64-row workgroups for the copies an expert can have.  Base pass: routed
-// experts widest bit-width first (their workgroups stream the most bytes),
-// R / rows-per-workgroup workgroups each; or the shared experts.
-WgMap stream_map(const moe_layer_t* L, bool shared, bool down, int nt) {
+// Work map of one launch (routed experts, or the shared experts).  The
+// switched-class workgroups per routed expert bound what its copies can need:
+// classes 1..3 of gate/up hold at most n_gate + n_up rows in three classes,
+// class 1 of down at most n_down rows.
+WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
   WgMap m{};
-  int n = 0, wg = 0;
-  auto add = [&](int e, int n_wg, int sw) {
-    if (n_wg <= 0) return;
-    m.e[n] = static_cast<int16_t>(e);
-    m.sw[n] = static_cast<int8_t>(sw);
-    m.first[n] = wg;
-    wg += n_wg;
-    n++;
-  };
+  constexpr int rows = kWaves * 16;
   const int E = L->n_experts;
   if (shared) {
-    for (int i = 0; i < L->n_shared; i++) {
-      const int e = E + i;
-      const int R = down ? L->d_model : L->d_ff_shared;
-      add(e, R / (kWaves * 16 * base_rt(L->bits_host[e], nt)), 0);
-    }
-  } else {
-    const int R = down ? L->d_model : L->d_ff;
-    int bound[MOE_MAX_EXPERTS] = {0};
-    for (int kd = down ? 2 : 0; kd <= (down ? 2 : 1); kd++) {
-      const moe_kind_desc_t& k = L->kind[kd];
-      for (int s = 0; s < k.n_slots; s++) {
-        const int e = k.copy_hdr_host ? k.copy_hdr_host[2 * s] : -1;
-        if (e >= 0 && e < E) bound[e]++;
-        else for (int x = 0; x < E; x++) bound[x] = R;   // headers unknown: any row
-      }
-    }
-    for (int e = 0; e < E; e++)
-      add(e, static_cast<int>(cdiv(std::min(R, bound[e]), kWaves * 16)), 1);
-    for (int b : {8, 4, 3, 2})
-      for (int e = 0; e < E; e++)
-        if (L->bits_host[e] == b) add(e, R / (kWaves * 16 * base_rt(b, nt)), 0);
+    m.e0 = E;
+    m.n_e = L->n_shared;
+    m.n_sw = 0;
+    m.per_e = (down ? L->d_model : L->d_ff_shared) / rows;
+    for (int i = 0; i < L->n_shared; i++) m.order[i] = static_cast<int16_t>(i);
+    return m;
   }
-  m.n = n;
-  m.first[n] = wg;
+  const int R = down ? L->d_model : L->d_ff;
+  m.e0 = 0;
+  m.n_e = E;
+  m.per_e = R / rows;
+  std::vector<int> nc[2];
+  for (int kk = 0; kk < (down ? 1 : 2); kk++) {
+    const moe_kind_desc_t& k = L->kind[down ? 2 : kk];
+    nc[kk].assign(E, 0);
+    for (int s = 0; s < k.n_slots; s++) {
+      const int e = k.copy_hdr_host ? k.copy_hdr_host[2 * s] : -1;
+      if (e >= 0 && e < E) nc[kk][e]++;
+      else std::fill(nc[kk].begin(), nc[kk].end(), R);   // headers unknown: any row
+    }
+    for (int e = 0; e < E; e++) nc[kk][e] = std::min(nc[kk][e], R);
+  }
+  int n_sw = 0;
+  for (int e = 0; e < E; e++) {
+    const int64_t need = down ? cdiv(nc[0][e], rows)
+                              : (nc[0][e] + nc[1][e] > 0 ? cdiv(nc[0][e] + nc[1][e], rows) + 2 : 0);
+    n_sw = std::max<int>(n_sw, static_cast<int>(std::min<int64_t>(need, cdiv(R, rows) + 3)));
+  }
+  m.n_sw = n_sw;
+  int n = 0;
+  for (int b : {8, 4, 3, 2})
+    for (int e = 0; e < E; e++)
+      if (L->bits_host[e] == b) m.order[n++] = static_cast<int16_t>(e);
   return m;
 }
 
@@ -754,16 +733,17 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   mark(ev, n_ev, 1, s);
   auto stream = [&](auto nk, const WgMap& m, int nt, int nsplit) {
     constexpr int NK = decltype(nk)::value;
-    if (m.n == 0 || m.first[m.n] == 0) return;
-    const dim3 grid(static_cast<unsigned>(m.first[m.n] * nsplit));
+    const int64_t n_wg = static_cast<int64_t>(m.n_e) * (m.n_sw + m.per_e);
+    if (n_wg == 0) return;
+    const dim3 grid(static_cast<unsigned>(n_wg * nsplit));
     if (nt == 1) hipLaunchKernelGGL((ffn_stream_kernel<NM, 1, NK>), grid, dim3(256), 0, s, a, m, nsplit);
     else if (nt == 2) hipLaunchKernelGGL((ffn_stream_kernel<NM, 2, NK>), grid, dim3(256), 0, s, a, m, nsplit);
     else hipLaunchKernelGGL((ffn_stream_kernel<NM, 4, NK>), grid, dim3(256), 0, s, a, m, nsplit);
   };
   using two = std::integral_constant<int, 2>;
   using one = std::integral_constant<int, 1>;
-  stream(two{}, stream_map(L, false, false, p.nt_routed), p.nt_routed, 1);
-  if (S > 0) stream(two{}, stream_map(L, true, false, p.nt_shared), p.nt_shared, 1);
+  stream(two{}, stream_map(L, false, false), p.nt_routed, 1);
+  if (S > 0) stream(two{}, stream_map(L, true, false), p.nt_shared, 1);
   mark(ev, n_ev, 2, s);
   {  // group sums of h, [max(f,fs)/g][rows]
     const int64_t n = static_cast<int64_t>(a.Tk) * (a.f / g) * (g / 8);
@@ -779,8 +759,8 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     }
   }
   mark(ev, n_ev, 3, s);
-  stream(one{}, stream_map(L, false, true, p.nt_routed), p.nt_routed, p.n_split);
-  if (S > 0) stream(one{}, stream_map(L, true, true, p.nt_shared), p.nt_shared, p.n_split);
+  stream(one{}, stream_map(L, false, true), p.nt_routed, p.n_split);
+  if (S > 0) stream(one{}, stream_map(L, true, true), p.nt_shared, p.n_split);
   mark(ev, n_ev, 4, s);
 }
 
@@ -826,7 +806,7 @@ int ffn_entry(const moe_layer_t* L, const uint16_t* x, int32_t T, int32_t k,
   a.bits = L->bits;
   a.order_gu = L->order_gu;
   a.order_dn = L->order_dn;
-  a.n_base = L->n_base;
+  a.class_cnt = L->class_cnt;
   a.x = x;
   a.offsets = offsets;
   a.perm = perm_token;
@@ -845,6 +825,25 @@ int ffn_entry(const moe_layer_t* L, const uint16_t* x, int32_t T, int32_t k,
   a.hsum = reinterpret_cast<float*>(w + p.xsum_bytes + p.h_bytes);
   a.o = o;
   a.split_stride = static_cast<int64_t>(T) * (k + L->n_shared) * L->d_model;
+  {  // sizes of the buffer resources; every one must stay below 2^31 bytes
+    const int64_t lim = int64_t{1} << 31;
+    const int64_t xb = static_cast<int64_t>(T) * L->d_model * 2;
+    if (xb >= lim || static_cast<int64_t>(p.h_bytes) >= lim || static_cast<int64_t>(p.xsum_bytes) >= lim ||
+        static_cast<int64_t>(p.hsum_bytes) >= lim)
+      return MOE_ERR_ARG;
+    a.x_bytes = static_cast<uint32_t>(xb);
+    a.h_bytes = static_cast<uint32_t>(p.h_bytes);
+    a.xsum_bytes = static_cast<uint32_t>(p.xsum_bytes);
+    a.hsum_bytes = static_cast<uint32_t>(p.hsum_bytes);
+    for (int kd = 0; kd < 3; kd++) {
+      const int64_t K = kd == MOE_KIND_DOWN ? L->d_ff : L->d_model;
+      const int64_t cb = static_cast<int64_t>(L->kind[kd].n_slots) * K;
+      const int64_t sb = static_cast<int64_t>(L->kind[kd].n_slots) * (K / L->group) * 4;
+      if (cb >= lim || sb >= lim) return MOE_ERR_ARG;
+      a.copy_bytes[kd] = static_cast<uint32_t>(cb);
+      a.copy_sz_bytes[kd] = static_cast<uint32_t>(sb);
+    }
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(const_cast<void**>(events));
   if (L->group == 128)

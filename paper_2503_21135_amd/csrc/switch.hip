@@ -35,10 +35,11 @@ scatter_slots_kernel(const int32_t* __restrict__ list, int n, const int32_t* __r
 
 // One workgroup (4 waves) per routed expert.  Class of row i:
 // bit 0 = row_slot_a[i] >= 0, bit 1 = row_slot_b[i] >= 0 (b may be NULL).
-// order lists class 0 rows ascending, then class 1, 2, 3.
+// order lists class 0 rows ascending, then class 1, 2, 3; class_cnt[4e + c]
+// receives the size of class c.
 __global__ void __launch_bounds__(256)
 order_kernel(const int32_t* __restrict__ rs_a, const int32_t* __restrict__ rs_b, int R,
-             int32_t* __restrict__ order, int32_t* __restrict__ n_base) {
+             int32_t* __restrict__ order, int32_t* __restrict__ class_cnt) {
   __shared__ int cnt[4];
   __shared__ int wave_cnt[4][4];
   __shared__ int start[4];
@@ -58,8 +59,8 @@ order_kernel(const int32_t* __restrict__ rs_a, const int32_t* __restrict__ rs_b,
   }
   for (int c = 0; c < 4; c++) atomicAdd(&cnt[c], local[c]);
   __syncthreads();
+  if (tid < 4) class_cnt[4 * e + tid] = cnt[tid];
   if (tid == 0) {
-    n_base[e] = cnt[0];
     start[0] = 0;
     for (int c = 1; c < 4; c++) start[c] = start[c - 1] + cnt[c - 1];
   }
@@ -102,7 +103,7 @@ extern "C" int moe_set_channel_switch(moe_layer_t* L, int32_t kind, const int32_
                                       int32_t n_on, void* stream) {
   using namespace moe;
   if (!L || L->n_experts <= 0 || L->d_model <= 0 || L->d_ff <= 0) return MOE_ERR_ARG;
-  if (!L->order_gu || !L->order_dn || !L->n_base) return MOE_ERR_ARG;
+  if (!L->order_gu || !L->order_dn || !L->class_cnt) return MOE_ERR_ARG;
   for (int kd = 0; kd < 3; kd++)
     if (!L->kind[kd].row_slot) return MOE_ERR_ARG;
   if (kind < -1 || kind > 2) return MOE_ERR_ARG;
@@ -148,10 +149,10 @@ extern "C" int moe_set_channel_switch(moe_layer_t* L, int32_t kind, const int32_
   if (kind != MOE_KIND_DOWN)
     hipLaunchKernelGGL(order_kernel, dim3(E), dim3(256), 0, s, L->kind[0].row_slot,
                        static_cast<const int32_t*>(L->kind[1].row_slot), L->d_ff, L->order_gu,
-                       L->n_base);
+                       L->class_cnt);
   if (kind == MOE_KIND_DOWN || kind == -1)
     hipLaunchKernelGGL(order_kernel, dim3(E), dim3(256), 0, s, L->kind[2].row_slot,
                        static_cast<const int32_t*>(nullptr), L->d_model, L->order_dn,
-                       L->n_base + E);
+                       L->class_cnt + 4 * E);
   return launch_status(s);
 }

@@ -89,11 +89,11 @@ class MoELayer:
             K.row_slot = kd["row_slot"].data_ptr()
         self.order_gu = torch.empty(E * cfg.d_ff, dtype=torch.int32, device=dev)
         self.order_dn = torch.empty(E * cfg.d_model, dtype=torch.int32, device=dev)
-        self.n_base = torch.empty(2 * E, dtype=torch.int32, device=dev)
+        self.class_cnt = torch.empty(8 * E, dtype=torch.int32, device=dev)
         self.staging = torch.empty(max_slots + 1, dtype=torch.int32, device=dev)
         desc.order_gu = self.order_gu.data_ptr()
         desc.order_dn = self.order_dn.data_ptr()
-        desc.n_base = self.n_base.data_ptr()
+        desc.class_cnt = self.class_cnt.data_ptr()
         desc.staging = self.staging.data_ptr()
         self.desc = desc
         api.moe_set_channel_switch(desc, -1, None)

@@ -114,7 +114,7 @@ def _fake_layer(n_slots=4, hdr=None):
         K.copy_codes = K.copy_sz = K.copy_hdr = FAKE.value
         K.copy_hdr_host = hdr.ctypes.data
         K.row_slot = FAKE.value
-    L.order_gu = L.order_dn = L.n_base = L.staging = FAKE.value
+    L.order_gu = L.order_dn = L.class_cnt = L.staging = FAKE.value
     return L, keep
 
 
