@@ -79,48 +79,77 @@ __device__ __forceinline__ int64_t h_row(const FfnArgs& a, int p) {
                   : static_cast<int64_t>(a.Tk) * a.f + static_cast<int64_t>(p - a.Tk) * a.fs;
 }
 
-__device__ __forceinline__ uint32_t pair8(uint32_t w, int hi) {
-  // bytes (c0, c2, c1, c3) -> bf16 pair (c0, c1) or (c2, c3), exact integers
-  const float a = hi ? static_cast<float>((w >> 8) & 0xFFu) : static_cast<float>(w & 0xFFu);
-  const float b = hi ? static_cast<float>(w >> 24) : static_cast<float>((w >> 16) & 0xFFu);
-  return (__float_as_uint(a) >> 16) | (__float_as_uint(b) & 0xFFFF0000u);
+// Dequantization into exact bf16 integers.  b <= 4: a code q OR-ed into the
+// mantissa of bf16 128.0 gives 128 + q; one v_and_or_b32 per output register
+// (two codes) after a shift.  The OR operand must sit in a vector register:
+// an instruction with three operands cannot take two literal constants here,
+// and with the constant as a literal the compiler splits the operation in
+// two.  `vm` holds 0x43004300 (two bf16 128.0) in a vector register.
+// 8-bit codes go through the byte-to-float converter (q exactly), and one
+// byte permute takes the upper halves (the bf16 patterns) of two floats.
+// 3-bit codes use two contractions: the 2-bit plane as 128 + lo and the
+// 1-bit plane as 512 + 4*hi (vh = 0x44004400, bf16 512.0, whose mantissa
+// step is 4), so the sum carries lo + 4*hi + 640.
+template <int B>
+constexpr int kPlanes = B == 3 ? 2 : 1;
+
+template <int B>
+constexpr float kOffset = B == 8 ? 0.f : (B == 3 ? 640.f : 128.f);
+
+__device__ __forceinline__ uint32_t andor(uint32_t x, uint32_t mask, uint32_t vm) {
+  return (x & mask) | vm;
+}
+
+// byte i of w as an fp32 bit pattern (selected as v_cvt_f32_ubyte<i>)
+__device__ __forceinline__ uint32_t ubyte_f32(uint32_t w, int i) {
+  return __float_as_uint(static_cast<float>((w >> (8 * i)) & 0xFFu));
+}
+
+__device__ __forceinline__ uint32_t pair8(uint32_t lo_f32, uint32_t hi_f32) {
+  // bf16 halves: low 16 bits <- upper half of lo_f32, high 16 <- upper half of hi_f32
+  return __builtin_amdgcn_perm(hi_f32, lo_f32, 0x07060302u);
 }
 
 // Codes of one lane's group share -> NM MFMA operands of 8 bf16 integers
-// each (128 + q for b <= 4, q for b = 8), in natural K order.
+// each per plane, in natural K order.
 template <int B, int NM, int NW>
-__device__ __forceinline__ void dequant_b(const uint32_t (&cw)[NW], u32x4 (&wf)[NM]) {
+__device__ __forceinline__ void dequant_b(const uint32_t (&cw)[NW], u32x4 (&wf)[kPlanes<B>][NM],
+                                          uint32_t vm, uint32_t vh) {
   if constexpr (B == 4) {
 #pragma unroll
     for (int m = 0; m < NM; m++) {
       const uint32_t w = cw[m];
-      wf[m] = u32x4{(w & 0x000F000Fu) | kMagic, ((w >> 4) & 0x000F000Fu) | kMagic,
-                    ((w >> 8) & 0x000F000Fu) | kMagic, ((w >> 12) & 0x000F000Fu) | kMagic};
+      wf[0][m] = u32x4{andor(w, 0x000F000Fu, vm), andor(w >> 4, 0x000F000Fu, vm),
+                       andor(w >> 8, 0x000F000Fu, vm), andor(w >> 12, 0x000F000Fu, vm)};
     }
   } else if constexpr (B == 2) {
 #pragma unroll
     for (int m = 0; m < NM; m++) {
-      const uint32_t w = cw[m >> 1] >> ((m & 1) * 8);
-      wf[m] = u32x4{(w & 0x00030003u) | kMagic, ((w >> 2) & 0x00030003u) | kMagic,
-                    ((w >> 4) & 0x00030003u) | kMagic, ((w >> 6) & 0x00030003u) | kMagic};
+      const uint32_t w = cw[m >> 1];
+      const int sh = (m & 1) * 8;
+      wf[0][m] = u32x4{andor(w >> sh, 0x00030003u, vm), andor(w >> (sh + 2), 0x00030003u, vm),
+                       andor(w >> (sh + 4), 0x00030003u, vm), andor(w >> (sh + 6), 0x00030003u, vm)};
     }
   } else if constexpr (B == 8) {
 #pragma unroll
-    for (int m = 0; m < NM; m++)
-      wf[m] = u32x4{pair8(cw[2 * m], 0), pair8(cw[2 * m], 1), pair8(cw[2 * m + 1], 0),
-                    pair8(cw[2 * m + 1], 1)};
-  } else {  // 3-bit planes, NM == 4
+    for (int m = 0; m < NM; m++) {
+      // bytes (c0, c2, c1, c3) of each word -> pairs (c0, c1), (c2, c3)
+      const uint32_t w0 = cw[2 * m], w1 = cw[2 * m + 1];
+      wf[0][m] = u32x4{pair8(ubyte_f32(w0, 0), ubyte_f32(w0, 2)), pair8(ubyte_f32(w0, 1), ubyte_f32(w0, 3)),
+                       pair8(ubyte_f32(w1, 0), ubyte_f32(w1, 2)), pair8(ubyte_f32(w1, 1), ubyte_f32(w1, 3))};
+    }
+  } else {  // 3-bit planes, NM == 4: words 0/1 the 2-bit plane, word 2 the 1-bit plane
 #pragma unroll
     for (int m = 0; m < NM; m++) {
-      uint32_t v[4];
+      uint32_t lo[4], hi[4];
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        const int p = 4 * m + j;
-        const uint32_t lo = (cw[p >> 3] >> (2 * (p & 7))) & 0x00030003u;
-        const uint32_t hi = ((cw[2] >> p) & 0x00010001u) << 2;
-        v[j] = lo | hi | kMagic;
+        const int p = 4 * m + j;   // output register: local codes 2p, 2p+1
+        lo[j] = andor(cw[p >> 3] >> (2 * (p & 7)), 0x00030003u, vm);
+        hi[j] = andor(cw[2] >> p, 0x00010001u, vh);
       }
-      wf[m] = u32x4{v[0], v[1], v[2], v[3]};
+      wf[0][m] = u32x4{lo[0], lo[1], lo[2], lo[3]};
+      wf[1][m] = u32x4{hi[0], hi[1], hi[2], hi[3]};
     }
   }
 }
@@ -140,38 +169,54 @@ constexpr uint32_t kOOB = 0x80000000u;   // past every resource: sizes are < 2^3
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
+// Values that are the same in every lane but were loaded from global memory
+// live in vector registers; a buffer resource built from them would need a
+// loop over lanes at every load.  These move such values to scalar registers.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t uni(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
+}
+__device__ __forceinline__ int64_t uni(int64_t v) {
+  const uint64_t u = static_cast<uint64_t>(v);
+  const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(u)));
+  const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(u >> 32)));
+  return static_cast<int64_t>(lo | (hi << 32));
+}
+
 __device__ __forceinline__ Rsrc make_rsrc(const void* p, uint32_t bytes) {
   // word 3 = 0x00020000: 32-bit data format, raw (unswizzled) addressing
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0),
                                            static_cast<int>(bytes), 0x00020000);
 }
 
-__device__ __forceinline__ u32x4 bload4(Rsrc r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+// Loads at byte offset off + soff of resource r; the range check applies to
+// `off`, so kOOB there reads zeros whatever the scalar offset `soff`.
+__device__ __forceinline__ u32x4 bload4(Rsrc r, uint32_t off, uint32_t soff = 0) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0);
 }
 
 template <int NW>
-__device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off) {
+__device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off, uint32_t soff) {
   if constexpr (NW == 8) {
-    const u32x4 a = bload4(r, off);
-    const u32x4 b = bload4(r, off + 16u);
+    const u32x4 a = bload4(r, off, soff);
+    const u32x4 b = bload4(r, off == kOOB ? kOOB : off + 16u, soff);
 #pragma unroll
     for (int i = 0; i < 4; i++) {
       cw[i] = a[i];
       cw[4 + i] = b[i];
     }
   } else if constexpr (NW == 4) {
-    const u32x4 a = bload4(r, off);
+    const u32x4 a = bload4(r, off, soff);
 #pragma unroll
     for (int i = 0; i < 4; i++) cw[i] = a[i];
   } else if constexpr (NW == 3) {
-    const auto a = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, 0);
+    const auto a = __builtin_amdgcn_raw_buffer_load_b96(r, off, soff, 0);
     cw[0] = a[0]; cw[1] = a[1]; cw[2] = a[2];
   } else if constexpr (NW == 2) {
-    const auto a = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    const auto a = __builtin_amdgcn_raw_buffer_load_b64(r, off, soff, 0);
     cw[0] = a[0]; cw[1] = a[1];
   } else {
-    cw[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    cw[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, soff, 0);
   }
 }
 
@@ -183,13 +228,18 @@ __device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off) 
 // source for all rows -- the expert's base codes at bit-width B, or the
 // cached 8-bit copies -- so the loads are wave-uniform in shape and the code
 // registers are sized for that width (template BG / BU).  The packed codes of
-// the next kStages groups are in flight in registers while the current group
+// the next kStages<BG, BU> groups are in flight in registers while the current group
 // is dequantized and contracted; the activations of the workgroup's token
 // tile (NT*16 rows) are staged in LDS two groups at a time (double-buffered,
 // one barrier per two groups), so every wave reads them from LDS.
 
 constexpr int kWaves = 4;
-constexpr int kStages = 4;   // groups of codes in flight per wave
+// Groups of codes in flight per wave.  The activations of chunk c+2 are
+// loaded while chunk c is contracted, so that waiting for them (vector loads
+// complete in order) never waits for a code load the loop does not already
+// need: with two-group chunks that holds for four groups in flight.
+template <int BG, int BU>
+constexpr int kStages = 4;
 
 // Work of one launch over experts e0 .. e0+n_e-1.  Every workgroup covers
 // kWaves*16 row positions of one source class of one expert.  Workgroups
@@ -214,8 +264,10 @@ struct Stage {
   uint32_t szw[RT][2];
 };
 
-// Source of one kind for a workgroup: resources, per-group strides and the
-// lane's byte offsets (kOOB for lanes past the rows of the class).
+// Source of one kind for a workgroup: resources over the expert's codes and
+// {scale, zero} words (or the copies), the per-group stride of the {s, z}
+// words and the lane's byte offsets (kOOB for lanes past the rows of the
+// class).  The per-group advance goes into the scalar offset of the loads.
 template <int RT>
 struct Src {
   Rsrc code, sz;
@@ -228,11 +280,12 @@ template <int NM, int B, int RT>
 __device__ __forceinline__ void load_kind(uint32_t (&cw)[RT][(kWords<NM, B>)], uint32_t (&szw)[RT],
                                           const Src<RT>& s, int gi, bool gv) {
   constexpr uint32_t gcb = NM * 32 * B / 8;   // code bytes per row and group
+  const uint32_t cadv = gv ? static_cast<uint32_t>(gi) * gcb : 0u;
+  const uint32_t sadv = gv ? static_cast<uint32_t>(gi) * s.sz_gstride : 0u;
 #pragma unroll
   for (int rt = 0; rt < RT; rt++) {
-    bload<kWords<NM, B>>(cw[rt], s.code, gv ? s.coff[rt] + gi * gcb : kOOB);
-    szw[rt] = __builtin_amdgcn_raw_buffer_load_b32(s.sz, gv ? s.soff[rt] + gi * s.sz_gstride : kOOB,
-                                                   0, 0);
+    bload<kWords<NM, B>>(cw[rt], s.code, gv ? s.coff[rt] : kOOB, cadv);
+    szw[rt] = __builtin_amdgcn_raw_buffer_load_b32(s.sz, gv ? s.soff[rt] : kOOB, sadv, 0);
   }
 }
 
@@ -258,36 +311,37 @@ __device__ __forceinline__ void load_stage(Stage<NM, RT, BG, BU>& st, const Src<
 // wait-state insertion was observed to fall short (the last accumulator
 // element was read stale).  The 3 x s_nop 7 (24 wait states) cover the
 // longest 16x16x32 bf16 MFMA latency on gfx950.
+template <int NM, int NT, int Bk>
+__device__ __forceinline__ void contract_kind(const uint32_t (&cw)[(kWords<NM, Bk>)], uint32_t szw,
+                                              const u32x4 (&af)[NT][NM], uint32_t vm, uint32_t vh,
+                                              f32x4 (&tmp)[NT], float& sc, float& zz) {
+  u32x4 wf[kPlanes<Bk>][NM];
+  dequant_b<Bk, NM, kWords<NM, Bk>>(cw, wf, vm, vh);
+  sc = fp16_bits_to_f32(szw & 0xFFFFu);
+  zz = fp16_bits_to_f32(szw >> 16) + kOffset<Bk>;
+#pragma unroll
+  for (int nt = 0; nt < NT; nt++) {
+    f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int m = 0; m < NM; m++)
+#pragma unroll
+      for (int pl = 0; pl < kPlanes<Bk>; pl++) t = mfma16(af[nt][m], wf[pl][m], t);
+    tmp[nt] = t;
+  }
+}
+
 template <int NM, int NT, int RT, int NK, int BG, int BU>
 __device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st,
                                               const u32x4 (&af)[NT][NM], const f32x4 (&X)[NT],
-                                              f32x4 (&acc)[RT][NK][NT]) {
+                                              uint32_t vm, uint32_t vh, f32x4 (&acc)[RT][NK][NT]) {
   f32x4 tmp[RT][NK][NT];
   float sc[RT][NK], zz[RT][NK];
 #pragma unroll
-  for (int rt = 0; rt < RT; rt++)
-#pragma unroll
-    for (int kk = 0; kk < NK; kk++) {
-      u32x4 wf[NM];
-      constexpr int Bk0 = BG, Bk1 = BU;
-      float off;
-      if (kk == 0) {
-        dequant_b<Bk0, NM, kWords<NM, Bk0>>(st.cg[rt], wf);
-        off = Bk0 == 8 ? 0.f : 128.f;
-      } else {
-        dequant_b<Bk1, NM, kWords<NM, Bk1>>(st.cu[rt], wf);
-        off = Bk1 == 8 ? 0.f : 128.f;
-      }
-      sc[rt][kk] = fp16_bits_to_f32(st.szw[rt][kk] & 0xFFFFu);
-      zz[rt][kk] = fp16_bits_to_f32(st.szw[rt][kk] >> 16) + off;
-#pragma unroll
-      for (int nt = 0; nt < NT; nt++) {
-        f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 0; m < NM; m++) t = mfma16(af[nt][m], wf[m], t);
-        tmp[rt][kk][nt] = t;
-      }
-    }
+  for (int rt = 0; rt < RT; rt++) {
+    contract_kind<NM, NT, BG>(st.cg[rt], st.szw[rt][0], af, vm, vh, tmp[rt][0], sc[rt][0], zz[rt][0]);
+    if constexpr (NK == 2)
+      contract_kind<NM, NT, BU>(st.cu[rt], st.szw[rt][1], af, vm, vh, tmp[rt][1], sc[rt][1], zz[rt][1]);
+  }
   __builtin_amdgcn_sched_barrier(0);
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
   __builtin_amdgcn_sched_barrier(0);
@@ -303,14 +357,21 @@ __device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st,
                                          acc[rt][kk][nt][i]);
 }
 
+// Groups per LDS chunk of activations.  (Four-group chunks halve the
+// barriers but double the tile's LDS, which limits the occupancy of the
+// down projection; two measured faster.)
+template <int NT>
+constexpr int kChunk = 2;
+
 template <int NM, int NT>
 struct XTile {
   static constexpr int g = NM * 32;
-  static constexpr int KC = 2 * g;   // K columns per LDS chunk (2 groups)
+  static constexpr int CG = kChunk<NT>;
+  static constexpr int KC = CG * g;   // K columns per LDS chunk
   static constexpr int TOK = NT * 16;
   static constexpr int LDW = KC + 8;  // row stride in bf16 (16-byte pad)
   uint16_t x[2][TOK][LDW];
-  float xs[2][2][TOK];
+  float xs[2][CG][TOK];
 };
 
 // The rows at order positions [pos0, pos1) of expert e (lanes past pos1
@@ -325,21 +386,24 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   constexpr int PIECES = TOK * KC / 8;   // 16-byte pieces per chunk
   constexpr int PPT = PIECES / 256;
   static_assert(PIECES % 256 == 0, "chunk must split evenly over the workgroup");
-  static_assert(kStages == 4, "the loop body below handles four groups");
+  constexpr int S = kStages<BG, BU>;
+  constexpr int CG = XTile<NM, NT>::CG;
+  static_assert(S == 4 && (CG == 2 || CG == 4), "the loop bodies below handle these");
+  static_assert(CG * TOK <= 256, "one thread per group-sum entry of a chunk");
   const int tid = threadIdx.x;
   const int wv = tid >> 6;
   const int lane = tid & 63;
   const int r16 = lane & 15;
   const int kq = lane >> 4;
-  const int seg0 = a.offsets[e];
-  const int seg1 = a.offsets[e + 1];
+  const int seg0 = uni(a.offsets[e]);
+  const int seg1 = uni(a.offsets[e + 1]);
   const bool routed = e < a.E;
   const bool down = NK == 1;
   const int K = down ? (routed ? a.f : a.fs) : a.d;
   const int G = K / g;
   const int g0 = sp * G / n_split;
   const int g1 = (sp + 1) * G / n_split;
-  const int be = a.bits[e];
+  const int be = uni(a.bits[e]);
   const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
 
@@ -354,30 +418,31 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   Src<RT> src[2];
 #pragma unroll
   for (int kk = 0; kk < NK; kk++) {
+    // scalar selects first, one resource each: a resource chosen by a branch
+    // would be merged in vector registers and force a loop per load
     const KindDev& kd = a.kd[kind0 + kk];
     const bool copy = (cls >> kk) & 1;
+    const uint32_t row_bytes = static_cast<uint32_t>(K) * be / 8;
+    const uint32_t words = static_cast<uint32_t>(g) * be / 128;   // per lane per group
+    const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
+                            : static_cast<const void*>(kd.codes + uni(kd.code_off[e]));
+    const void* sptr = copy ? static_cast<const void*>(kd.copy_sz)
+                            : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
+    const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
+    const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
     Src<RT>& s = src[kk];
-    if (!copy) {
-      const uint32_t row_bytes = static_cast<uint32_t>(K) * be / 8;
-      const uint32_t words = static_cast<uint32_t>(g) * be / 128;   // per lane per group
-      s.code = make_rsrc(kd.codes + kd.code_off[e], static_cast<uint32_t>(R) * row_bytes);
-      s.sz = make_rsrc(kd.sz + kd.sz_off[e], static_cast<uint32_t>(R) * G * 4u);
-      s.sz_gstride = static_cast<uint32_t>(R) * 4u;
+    s.code = make_rsrc(cptr, cbytes);
+    s.sz = make_rsrc(sptr, sbytes);
+    s.sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
 #pragma unroll
-      for (int rt = 0; rt < RT; rt++) {
-        s.coff[rt] = live[rt] ? row_id[rt] * row_bytes + kq * words * 4u : kOOB;
-        s.soff[rt] = live[rt] ? row_id[rt] * 4u : kOOB;
-      }
-    } else {
-      s.code = make_rsrc(kd.copy_codes, a.copy_bytes[kind0 + kk]);
-      s.sz = make_rsrc(kd.copy_sz, a.copy_sz_bytes[kind0 + kk]);
-      s.sz_gstride = 4u;
-#pragma unroll
-      for (int rt = 0; rt < RT; rt++) {
-        const int slot = live[rt] ? kd.row_slot[static_cast<int64_t>(e) * R + row_id[rt]] : -1;
-        s.coff[rt] = slot >= 0 ? static_cast<uint32_t>(slot) * K + kq * (g / 4) : kOOB;
-        s.soff[rt] = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
-      }
+    for (int rt = 0; rt < RT; rt++) {
+      const int slot = (copy && live[rt]) ? kd.row_slot[static_cast<int64_t>(e) * R + row_id[rt]] : -1;
+      const uint32_t c_base = live[rt] ? row_id[rt] * row_bytes + kq * words * 4u : kOOB;
+      const uint32_t s_base = live[rt] ? row_id[rt] * 4u : kOOB;
+      const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * K + kq * (g / 4) : kOOB;
+      const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
+      s.coff[rt] = copy ? c_copy : c_base;
+      s.soff[rt] = copy ? s_copy : s_base;
     }
   }
   const float* xsum = down ? a.hsum : a.xsum;
@@ -395,22 +460,28 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
                          : kOOB;
     }
     const int acol = (tid % (KC / 8)) * 8;   // same column for every piece of a thread
-    const int xs_g = tid / TOK, xs_j = tid % TOK;   // xsum entry of threads < 2*TOK
-    const bool xs_live = tid < 2 * TOK && t0 + xs_j < seg1;
-    auto stage_x = [&](u32x4 (&v)[PPT], float& xsv, int gc) {
-      const bool in_k = gc + acol / g < g1;   // the chunk's second group may not exist
 #pragma unroll
-      for (int i = 0; i < PPT; i++)
-        v[i] = bload4(xr, (in_k && arow[i] != kOOB) ? arow[i] + 2u * (gc * g + acol) : kOOB);
-      const bool ok = xs_live && gc + xs_g < g1;
-      xsv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-          xsr, ok ? 4u * static_cast<uint32_t>((gc + xs_g) * a.rows + t0 + xs_j) : kOOB, 0, 0));
+    for (int i = 0; i < PPT; i++)
+      if (arow[i] != kOOB) arow[i] += 2u * acol;
+    const int xs_g = tid / TOK, xs_j = tid % TOK;   // xsum entry of threads < CG*TOK
+    const uint32_t xs_off = tid < CG * TOK && t0 + xs_j < seg1
+                                ? 4u * static_cast<uint32_t>(xs_g * a.rows + t0 + xs_j) : kOOB;
+    // chunk [gc, gc+CG): the chunk's first column / group goes into the scalar offset
+    auto stage_x = [&](u32x4 (&v)[PPT], float& xsv, int gc) {
+      const bool live_c = gc < g1;
+      const uint32_t xadv = live_c ? 2u * static_cast<uint32_t>(gc * g) : 0u;
+      const uint32_t sadv = live_c ? 4u * static_cast<uint32_t>(gc * a.rows) : 0u;
+      const bool in_k = gc + acol / g < g1;   // the chunk's later groups may not exist
+#pragma unroll
+      for (int i = 0; i < PPT; i++) v[i] = bload4(xr, in_k ? arow[i] : kOOB, xadv);
+      const bool ok = gc + xs_g < g1;
+      xsv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xsr, ok ? xs_off : kOOB, sadv, 0));
     };
     auto write_x = [&](const u32x4 (&v)[PPT], float xsv, int buf) {
 #pragma unroll
       for (int i = 0; i < PPT; i++)
         *reinterpret_cast<u32x4*>(&tl.x[buf][(tid + 256 * i) / (KC / 8)][acol]) = v[i];
-      if (tid < 2 * TOK) tl.xs[buf][xs_g][xs_j] = xsv;
+      if (tid < CG * TOK) tl.xs[buf][xs_g][xs_j] = xsv;
     };
 
     f32x4 acc[RT][NK][NT];
@@ -421,15 +492,17 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
 #pragma unroll
         for (int nt = 0; nt < NT; nt++) acc[rt][kk][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    Stage<NM, RT, BG, BU> st[kStages];
+    // dequantization constants, kept in vector registers (see dequant_b)
+    uint32_t vm = kMagic, vh = 0x44004400u;
+    asm volatile("" : "+v"(vm), "+v"(vh));
+    Stage<NM, RT, BG, BU> st[S];
 #pragma unroll
-    for (int s = 0; s < kStages; s++) load_stage<NM, RT, NK, BG, BU>(st[s], src, g0 + s, g0 + s < g1);
-    {
-      u32x4 v[PPT];
-      float xsv;
-      stage_x(v, xsv, g0);
-      write_x(v, xsv, 0);
-    }
+    for (int s = 0; s < S; s++) load_stage<NM, RT, NK, BG, BU>(st[s], src, g0 + s, g0 + s < g1);
+    u32x4 vx[CG == 2 ? 2 : 1][PPT];   // activations of the next chunk(s)
+    float vxs[CG == 2 ? 2 : 1];
+    stage_x(vx[0], vxs[0], g0);
+    write_x(vx[0], vxs[0], 0);
+    if constexpr (CG == 2) stage_x(vx[1], vxs[1], g0 + 2);
     __syncthreads();
     auto group = [&](Stage<NM, RT, BG, BU>& s, int buf, int gg, int gi) {
       if (gi < g1) {   // wave-uniform; the loads below are unconditional
@@ -443,23 +516,39 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
                 &tl.x[buf][nt * 16 + r16][gg * g + kq * (g / 4) + 8 * m]);
           X[nt] = *reinterpret_cast<const f32x4*>(&tl.xs[buf][gg][nt * 16 + 4 * kq]);
         }
-        compute_group<NM, NT, RT, NK, BG, BU>(s, af, X, acc);
+        compute_group<NM, NT, RT, NK, BG, BU>(s, af, X, vm, vh, acc);
       }
-      load_stage<NM, RT, NK, BG, BU>(s, src, gi + kStages, gi + kStages < g1);
+      load_stage<NM, RT, NK, BG, BU>(s, src, gi + S, gi + S < g1);
     };
-    for (int gc = g0; gc < g1; gc += 4) {
-      u32x4 vn[PPT];
-      float xsn;
-      stage_x(vn, xsn, gc + 2);
-      group(st[0], 0, 0, gc);
-      group(st[1], 0, 1, gc + 1);
-      write_x(vn, xsn, 1);
-      __syncthreads();
-      stage_x(vn, xsn, gc + 4);
-      group(st[2], 1, 0, gc + 2);
-      group(st[3], 1, 1, gc + 3);
-      write_x(vn, xsn, 0);
-      __syncthreads();
+    if constexpr (CG == 4) {
+      // One chunk = the four groups in flight: the activations of chunk c+1
+      // are loaded at the start of chunk c; every code load issued before
+      // them is for a group of chunk c, so waiting for them costs nothing.
+      for (int gc = g0; gc < g1; gc += 2 * CG) {
+#pragma unroll
+        for (int c = 0; c < 2; c++) {   // chunk c of the iteration sits in LDS buffer c
+          const int gb = gc + c * CG;
+          stage_x(vx[0], vxs[0], gb + CG);
+#pragma unroll
+          for (int j = 0; j < CG; j++) group(st[j], c, j, gb + j);
+          write_x(vx[0], vxs[0], c ^ 1);
+          __syncthreads();
+        }
+      }
+    } else {
+      // Two-group chunks: the activations are loaded two chunks ahead, so
+      // that waiting for them never waits for a code load of a later group.
+      for (int gc = g0; gc < g1; gc += S) {
+#pragma unroll
+        for (int c = 0; c < 2; c++) {   // chunk c of the iteration sits in LDS buffer c
+          // vx[c] held chunk gc+2c (written to LDS already); reuse it for gc+2c+4
+          stage_x(vx[c], vxs[c], gc + 2 * c + 4);
+          group(st[2 * c], c, 0, gc + 2 * c);
+          group(st[2 * c + 1], c, 1, gc + 2 * c + 1);
+          write_x(vx[c ^ 1], vxs[c ^ 1], c ^ 1);   // chunk gc+2c+2, loaded one chunk ago
+          __syncthreads();
+        }
+      }
     }
 
     if constexpr (NK == 2) {
@@ -528,32 +617,35 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
     blk = j % map.per_e;
     cls = 0;
   }
-  if (a.offsets[e + 1] <= a.offsets[e]) return;
+  if (uni(a.offsets[e + 1]) <= uni(a.offsets[e])) return;
   const bool routed = e < a.E;
   const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
   int start = 0, count = R;
   if (routed) {
     const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+    int cnt[4];
+#pragma unroll
+    for (int c = 0; c < 4; c++) cnt[c] = uni(cc[c]);
     if (wgi < n_swg) {   // find the switched class of this workgroup
-      start = cc[0];
+      start = cnt[0];
       cls = 4;
       for (int c = 1; c < (NK == 1 ? 2 : 4); c++) {
-        const int nwg = (cc[c] + rows - 1) / rows;
+        const int nwg = (cnt[c] + rows - 1) / rows;
         if (blk < nwg) {
           cls = c;
           break;
         }
         blk -= nwg;
-        start += cc[c];
+        start += cnt[c];
       }
       if (cls == 4) return;
     }
-    count = cc[cls];
+    count = cnt[cls];
   }
   const int pos0 = start + blk * rows;
   if (blk * rows >= count) return;
   const int pos1 = min(pos0 + rows, start + count);
-  const int B = a.bits[e];
+  const int B = uni(a.bits[e]);
   if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
