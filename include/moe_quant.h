@@ -97,18 +97,30 @@ extern "C" {
 #define MOE_KIND_DOWN 2   /* [d_model][d_ff]  rows = output channels, K = d_ff   */
 
 /*
+ * moe_code_row_words -- row stride, in 32-bit words, of the packed code
+ * matrices moe_expert_ffn_mixed reads (base codes and 8-bit copies): K*bits/32
+ * words of codes followed by padding of 16 words (32 words at bits == 8), so
+ * that consecutive rows never start a power of two of bytes apart.  The
+ * padding words are never read.  Returns 0 for bits outside {2, 3, 4, 8} or
+ * K not a positive multiple of 128.
+ */
+int64_t moe_code_row_words(int32_t K, int32_t bits);
+
+/*
  * One kind (gate, up or down) of every expert of a layer.
  *
  * Base codes: expert e (routed experts 0..E-1 first, then shared experts
  * E..E+S-1) stores its R_e x K_e matrix row-major in the packed layout above
- * at word offset code_off[e] of `codes` (row stride K_e*bits[e]/32 words).
+ * at word offset code_off[e] of `codes`, row stride
+ * moe_code_row_words(K_e, bits[e]) words.
  * code_off[e] must be a multiple of 4 (16-byte aligned rows start).
  * Its scales and zeros are group-major: the {s16, z} word of (row r, group j)
  * is sz[sz_off[e] + j*R_e + r].
  *
  * Resident 8-bit copies (the channel cache of Sec. IV-B / V-A, kept here as
  * 8-bit codes quantized from the original fp32 rows): slot s holds one row of
- * a routed expert, K/4 words at copy_codes[s*(K/4)], its {s16, z} words at
+ * a routed expert, K/4 words at copy_codes[s*moe_code_row_words(K, 8)], its
+ * {s16, z} words at
  * copy_sz[s*(K/group) + j], and its header (expert, row) at copy_hdr[2s],
  * copy_hdr[2s+1].  A layer may have n_slots = 0 (copy pointers then NULL).
  *

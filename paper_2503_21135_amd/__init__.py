@@ -8,7 +8,7 @@ The compute lives in libmoe_quant.so (built by ``build.build()``); the
 modules here only marshal torch tensors into it.
 """
 from ._lib import EXPORTS, LIB_PATH, MoEError, load  # noqa: F401
-from .api import (moe_expert_ffn_mixed, moe_expert_ffn_mixed_ev, moe_ffn_plan, moe_quant_pack,  # noqa: F401
-                  moe_route_permute, moe_route_workspace_bytes, moe_set_channel_switch,
+from .api import (moe_code_row_words, moe_expert_ffn_mixed, moe_expert_ffn_mixed_ev,  # noqa: F401
+                  moe_ffn_plan, moe_quant_pack, moe_route_permute, moe_route_workspace_bytes, moe_set_channel_switch,
                   moe_unpermute_combine)
 from .layer import MoELayer  # noqa: F401

@@ -18,7 +18,8 @@ MAX_EXPERTS = 256
 MAX_TOPK = 16
 
 EXPORTS = (
-    "moe_quant_pack", "moe_route_permute", "moe_route_workspace_bytes", "moe_ffn_plan",
+    "moe_quant_pack", "moe_code_row_words", "moe_route_permute", "moe_route_workspace_bytes",
+    "moe_ffn_plan",
     "moe_expert_ffn_mixed", "moe_expert_ffn_mixed_ev", "moe_set_channel_switch",
     "moe_unpermute_combine", "moe_status_str",
 )
@@ -66,6 +67,7 @@ def load() -> C.CDLL:
         "moe_route_permute": (C.c_int, [vp, i32, i32, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp,
                                         vp, sz_t, vp]),
         "moe_route_workspace_bytes": (sz_t, [i32, i32, i32, i32]),
+        "moe_code_row_words": (i64, [i32, i32]),
         "moe_ffn_plan": (C.c_int, [C.POINTER(LayerDesc), i32, i32, C.POINTER(i32), C.POINTER(sz_t)]),
         "moe_expert_ffn_mixed": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
                                            sz_t, vp]),

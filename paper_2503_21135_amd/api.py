@@ -50,6 +50,14 @@ def moe_quant_pack(w: torch.Tensor, bits: int, group: int, codes: torch.Tensor,
     check(st, "moe_quant_pack")
 
 
+def moe_code_row_words(K: int, bits: int) -> int:
+    """Row stride (32-bit words) of packed code matrices read by the FFN."""
+    n = int(load().moe_code_row_words(K, bits))
+    if n <= 0:
+        raise MoEError("moe_code_row_words: bad K=%d or bits=%d" % (K, bits))
+    return n
+
+
 def moe_route_workspace_bytes(T: int, E: int, k: int, S: int) -> int:
     return int(load().moe_route_workspace_bytes(T, E, k, S))
 

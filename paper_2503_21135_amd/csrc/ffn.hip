@@ -234,12 +234,14 @@ __device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off, 
 // one barrier per two groups), so every wave reads them from LDS.
 
 constexpr int kWaves = 4;
-// Groups of codes in flight per wave.  The activations of chunk c+2 are
-// loaded while chunk c is contracted, so that waiting for them (vector loads
-// complete in order) never waits for a code load the loop does not already
-// need: with two-group chunks that holds for four groups in flight.
+// Groups of codes in flight per wave: four, or two when a kind streams 8-bit
+// codes (the same bytes in flight in half the registers).  The activations
+// of chunk c+2 are loaded while chunk c is contracted, so that waiting for
+// them (vector loads complete in order) never waits for a code load the loop
+// does not already need: with two-group chunks that holds for up to four
+// groups in flight.
 template <int BG, int BU>
-constexpr int kStages = 4;
+constexpr int kStages = (BG == 8 || BU == 8) ? 2 : 4;
 
 // Work of one launch over experts e0 .. e0+n_e-1.  Every workgroup covers
 // kWaves*16 row positions of one source class of one expert.  Workgroups
@@ -252,6 +254,15 @@ struct WgMap {
   int n_sw;
   int per_e;
   int16_t order[MOE_MAX_EXPERTS];
+  int8_t bits[MOE_MAX_EXPERTS];   // bits[e - e0]
+};
+
+// Metadata a workgroup loads in its prologue, all issued before any is
+// waited for (a chain of dependent loads at the start of every workgroup
+// costs more than the loads themselves).
+struct Pre {
+  int64_t code_off[2], sz_off[2];   // per kind of the launch
+  int row0;                         // class 0: this lane's row of the order
 };
 
 template <int NM, int B>
@@ -360,13 +371,12 @@ __device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st,
 // Groups per LDS chunk of activations.  (Four-group chunks halve the
 // barriers but double the tile's LDS, which limits the occupancy of the
 // down projection; two measured faster.)
-template <int NT>
 constexpr int kChunk = 2;
 
 template <int NM, int NT>
 struct XTile {
   static constexpr int g = NM * 32;
-  static constexpr int CG = kChunk<NT>;
+  static constexpr int CG = kChunk;
   static constexpr int KC = CG * g;   // K columns per LDS chunk
   static constexpr int TOK = NT * 16;
   static constexpr int LDW = KC + 8;  // row stride in bf16 (16-byte pad)
@@ -378,8 +388,8 @@ struct XTile {
 // idle), class cls (bit kk set: kind kk reads the 8-bit copies), token tile
 // passes over the expert's segment, K groups [g0, g1) of split sp.
 template <int NM, int NT, int RT, int NK, int BG, int BU>
-__device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, int e, int cls, int pos0, int pos1,
-                            int R, int sp, int n_split) {
+__device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, const Pre& pre, int e,
+                                            int cls, int pos0, int pos1, int R, int sp, int n_split) {
   constexpr int g = NM * 32;
   constexpr int KC = XTile<NM, NT>::KC;
   constexpr int TOK = XTile<NM, NT>::TOK;
@@ -388,7 +398,7 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   static_assert(PIECES % 256 == 0, "chunk must split evenly over the workgroup");
   constexpr int S = kStages<BG, BU>;
   constexpr int CG = XTile<NM, NT>::CG;
-  static_assert(S == 4 && (CG == 2 || CG == 4), "the loop bodies below handle these");
+  static_assert((S == 2 || S == 4) && CG == 2, "the loop body below handles two two-group chunks");
   static_assert(CG * TOK <= 256, "one thread per group-sum entry of a chunk");
   const int tid = threadIdx.x;
   const int wv = tid >> 6;
@@ -403,7 +413,7 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   const int G = K / g;
   const int g0 = sp * G / n_split;
   const int g1 = (sp + 1) * G / n_split;
-  const int be = uni(a.bits[e]);
+  const int be = BG == BU ? BG : (cls == 1 ? BU : BG);   // the base width of the expert
   const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
 
@@ -413,7 +423,8 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   for (int rt = 0; rt < RT; rt++) {
     const int pos = pos0 + wv * 16 * RT + rt * 16 + r16;
     live[rt] = pos < pos1;
-    row_id[rt] = live[rt] ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+    const int prow = (RT == 1 && cls == 0) ? pre.row0 : order[static_cast<int64_t>(e) * R + pos];
+    row_id[rt] = live[rt] ? (routed ? prow : pos) : 0;
   }
   Src<RT> src[2];
 #pragma unroll
@@ -422,12 +433,12 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
     // would be merged in vector registers and force a loop per load
     const KindDev& kd = a.kd[kind0 + kk];
     const bool copy = (cls >> kk) & 1;
-    const uint32_t row_bytes = static_cast<uint32_t>(K) * be / 8;
+    const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
     const uint32_t words = static_cast<uint32_t>(g) * be / 128;   // per lane per group
     const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
-                            : static_cast<const void*>(kd.codes + uni(kd.code_off[e]));
+                            : static_cast<const void*>(kd.codes + uni(pre.code_off[kk]));
     const void* sptr = copy ? static_cast<const void*>(kd.copy_sz)
-                            : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
+                            : static_cast<const void*>(kd.sz + uni(pre.sz_off[kk]));
     const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
     const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
     Src<RT>& s = src[kk];
@@ -439,7 +450,9 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
       const int slot = (copy && live[rt]) ? kd.row_slot[static_cast<int64_t>(e) * R + row_id[rt]] : -1;
       const uint32_t c_base = live[rt] ? row_id[rt] * row_bytes + kq * words * 4u : kOOB;
       const uint32_t s_base = live[rt] ? row_id[rt] * 4u : kOOB;
-      const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * K + kq * (g / 4) : kOOB;
+      const uint32_t c_copy =
+          slot >= 0 ? static_cast<uint32_t>(slot) * 4u * static_cast<uint32_t>(code_row_words(K, 8)) + kq * (g / 4)
+                    : kOOB;
       const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
       s.coff[rt] = copy ? c_copy : c_base;
       s.soff[rt] = copy ? s_copy : s_base;
@@ -512,42 +525,22 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
         for (int nt = 0; nt < NT; nt++) {
 #pragma unroll
           for (int m = 0; m < NM; m++)
-            af[nt][m] = *reinterpret_cast<const u32x4*>(
-                &tl.x[buf][nt * 16 + r16][gg * g + kq * (g / 4) + 8 * m]);
+            af[nt][m] = *reinterpret_cast<const u32x4*>(&tl.x[buf][nt * 16 + r16][gg * g + kq * (g / 4) + 8 * m]);
           X[nt] = *reinterpret_cast<const f32x4*>(&tl.xs[buf][gg][nt * 16 + 4 * kq]);
         }
         compute_group<NM, NT, RT, NK, BG, BU>(s, af, X, vm, vh, acc);
       }
       load_stage<NM, RT, NK, BG, BU>(s, src, gi + S, gi + S < g1);
     };
-    if constexpr (CG == 4) {
-      // One chunk = the four groups in flight: the activations of chunk c+1
-      // are loaded at the start of chunk c; every code load issued before
-      // them is for a group of chunk c, so waiting for them costs nothing.
-      for (int gc = g0; gc < g1; gc += 2 * CG) {
+    for (int gc = g0; gc < g1; gc += 4) {
 #pragma unroll
-        for (int c = 0; c < 2; c++) {   // chunk c of the iteration sits in LDS buffer c
-          const int gb = gc + c * CG;
-          stage_x(vx[0], vxs[0], gb + CG);
-#pragma unroll
-          for (int j = 0; j < CG; j++) group(st[j], c, j, gb + j);
-          write_x(vx[0], vxs[0], c ^ 1);
-          __syncthreads();
-        }
-      }
-    } else {
-      // Two-group chunks: the activations are loaded two chunks ahead, so
-      // that waiting for them never waits for a code load of a later group.
-      for (int gc = g0; gc < g1; gc += S) {
-#pragma unroll
-        for (int c = 0; c < 2; c++) {   // chunk c of the iteration sits in LDS buffer c
-          // vx[c] held chunk gc+2c (written to LDS already); reuse it for gc+2c+4
-          stage_x(vx[c], vxs[c], gc + 2 * c + 4);
-          group(st[2 * c], c, 0, gc + 2 * c);
-          group(st[2 * c + 1], c, 1, gc + 2 * c + 1);
-          write_x(vx[c ^ 1], vxs[c ^ 1], c ^ 1);   // chunk gc+2c+2, loaded one chunk ago
-          __syncthreads();
-        }
+      for (int c = 0; c < 2; c++) {   // chunk c of the iteration sits in LDS buffer c
+        // vx[c] held chunk gc+2c (written to LDS already); reuse it for gc+2c+4
+        stage_x(vx[c], vxs[c], gc + 2 * c + 4);
+        group(st[(2 * c) % S], c, 0, gc + 2 * c);
+        group(st[(2 * c + 1) % S], c, 1, gc + 2 * c + 1);
+        write_x(vx[c ^ 1], vxs[c ^ 1], c ^ 1);   // chunk gc+2c+2, loaded one chunk ago
+        __syncthreads();
       }
     }
 
@@ -582,16 +575,16 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
 
 
 template <int NM, int NT, int NK, int B>
-__device__ __forceinline__ void dispatch_class(const FfnArgs& a, XTile<NM, NT>& tl, int e, int cls,
-                                               int pos0, int pos1, int R, int sp, int n_split) {
+__device__ __forceinline__ void dispatch_class(const FfnArgs& a, XTile<NM, NT>& tl, const Pre& pre, int e,
+                                               int cls, int pos0, int pos1, int R, int sp, int n_split) {
   if constexpr (NK == 1) {
-    if (cls == 0) stream_body<NM, NT, 1, 1, B, B>(a, tl, e, 0, pos0, pos1, R, sp, n_split);
-    else stream_body<NM, NT, 1, 1, 8, 8>(a, tl, e, 1, pos0, pos1, R, sp, n_split);
+    if (cls == 0) stream_body<NM, NT, 1, 1, B, B>(a, tl, pre, e, 0, pos0, pos1, R, sp, n_split);
+    else stream_body<NM, NT, 1, 1, 8, 8>(a, tl, pre, e, 1, pos0, pos1, R, sp, n_split);
   } else {
-    if (cls == 0) stream_body<NM, NT, 1, 2, B, B>(a, tl, e, 0, pos0, pos1, R, sp, n_split);
-    else if (cls == 1) stream_body<NM, NT, 1, 2, 8, B>(a, tl, e, 1, pos0, pos1, R, sp, n_split);
-    else if (cls == 2) stream_body<NM, NT, 1, 2, B, 8>(a, tl, e, 2, pos0, pos1, R, sp, n_split);
-    else stream_body<NM, NT, 1, 2, 8, 8>(a, tl, e, 3, pos0, pos1, R, sp, n_split);
+    if (cls == 0) stream_body<NM, NT, 1, 2, B, B>(a, tl, pre, e, 0, pos0, pos1, R, sp, n_split);
+    else if (cls == 1) stream_body<NM, NT, 1, 2, 8, B>(a, tl, pre, e, 1, pos0, pos1, R, sp, n_split);
+    else if (cls == 2) stream_body<NM, NT, 1, 2, B, 8>(a, tl, pre, e, 2, pos0, pos1, R, sp, n_split);
+    else stream_body<NM, NT, 1, 2, 8, 8>(a, tl, pre, e, 3, pos0, pos1, R, sp, n_split);
   }
 }
 
@@ -617,15 +610,30 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
     blk = j % map.per_e;
     cls = 0;
   }
-  if (uni(a.offsets[e + 1]) <= uni(a.offsets[e])) return;
   const bool routed = e < a.E;
   const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
+  const int kind0 = NK == 1 ? 2 : 0;
+  // issue every metadata load of the workgroup before waiting for any of them
+  const int32_t* ccp = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * (routed ? e : 0);
+  const int o0 = a.offsets[e], o1 = a.offsets[e + 1];
+  int cnt[4];
+#pragma unroll
+  for (int c = 0; c < 4; c++) cnt[c] = ccp[c];
+  Pre pre;
+#pragma unroll
+  for (int kk = 0; kk < NK; kk++) {
+    pre.code_off[kk] = a.kd[kind0 + kk].code_off[e];
+    pre.sz_off[kk] = a.kd[kind0 + kk].sz_off[e];
+  }
+  const int32_t* order = NK == 1 ? a.order_dn : a.order_gu;
+  pre.row0 = (routed && wgi >= n_swg)
+                 ? order[static_cast<int64_t>(e) * R + blk * rows + (threadIdx.x >> 6) * 16 + (threadIdx.x & 15)]
+                 : 0;
+  if (uni(o1) <= uni(o0)) return;
   int start = 0, count = R;
   if (routed) {
-    const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
-    int cnt[4];
 #pragma unroll
-    for (int c = 0; c < 4; c++) cnt[c] = uni(cc[c]);
+    for (int c = 0; c < 4; c++) cnt[c] = uni(cnt[c]);
     if (wgi < n_swg) {   // find the switched class of this workgroup
       start = cnt[0];
       cls = 4;
@@ -645,11 +653,11 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
   const int pos0 = start + blk * rows;
   if (blk * rows >= count) return;
   const int pos1 = min(pos0 + rows, start + count);
-  const int B = uni(a.bits[e]);
-  if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
-  else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
-  else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
-  else if constexpr (NM == 4) dispatch_class<NM, NT, NK, 3>(a, tl, e, cls, pos0, pos1, R, sp, n_split);
+  const int B = map.bits[e - map.e0];
+  if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  else if constexpr (NM == 4) dispatch_class<NM, NT, NK, 3>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
 }
 
 // ------------------------------------------------------------------ group sums
@@ -740,7 +748,8 @@ int validate_layer(const moe_layer_t* L) {
   // buffer resources address each expert's codes and {scale, zero} words with
   // 32-bit byte offsets below 2^31
   const int64_t fm = std::max<int64_t>(L->d_ff, S > 0 ? L->d_ff_shared : 0);
-  if (fm * L->d_model >= (int64_t{1} << 31) / 4) return MOE_ERR_ARG;
+  if (fm * 4 * code_row_words(std::max<int64_t>(fm, L->d_model), 8) >= (int64_t{1} << 31))
+    return MOE_ERR_ARG;
   for (int e = 0; e < E + S; e++) {
     if (!valid_bits(L->bits_host[e])) return MOE_ERR_BITS;
     if (L->bits_host[e] == 3 && L->group != 128) return MOE_ERR_ARG;
@@ -774,7 +783,10 @@ WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
     m.n_e = L->n_shared;
     m.n_sw = 0;
     m.per_e = (down ? L->d_model : L->d_ff_shared) / rows;
-    for (int i = 0; i < L->n_shared; i++) m.order[i] = static_cast<int16_t>(i);
+    for (int i = 0; i < L->n_shared; i++) {
+      m.order[i] = static_cast<int16_t>(i);
+      m.bits[i] = static_cast<int8_t>(L->bits_host[E + i]);
+    }
     return m;
   }
   const int R = down ? L->d_model : L->d_ff;
@@ -799,6 +811,7 @@ WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
     n_sw = std::max<int>(n_sw, static_cast<int>(std::min<int64_t>(need, cdiv(R, rows) + 3)));
   }
   m.n_sw = n_sw;
+  for (int e = 0; e < E; e++) m.bits[e] = static_cast<int8_t>(L->bits_host[e]);
   int n = 0;
   for (int b : {8, 4, 3, 2})
     for (int e = 0; e < E; e++)
@@ -929,7 +942,7 @@ int ffn_entry(const moe_layer_t* L, const uint16_t* x, int32_t T, int32_t k,
     a.hsum_bytes = static_cast<uint32_t>(p.hsum_bytes);
     for (int kd = 0; kd < 3; kd++) {
       const int64_t K = kd == MOE_KIND_DOWN ? L->d_ff : L->d_model;
-      const int64_t cb = static_cast<int64_t>(L->kind[kd].n_slots) * K;
+      const int64_t cb = static_cast<int64_t>(L->kind[kd].n_slots) * 4 * code_row_words(K, 8);
       const int64_t sb = static_cast<int64_t>(L->kind[kd].n_slots) * (K / L->group) * 4;
       if (cb >= lim || sb >= lim) return MOE_ERR_ARG;
       a.copy_bytes[kd] = static_cast<uint32_t>(cb);

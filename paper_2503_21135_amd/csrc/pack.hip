@@ -145,3 +145,8 @@ extern "C" const char* moe_status_str(int status) {
     default: return "unknown status";
   }
 }
+
+extern "C" int64_t moe_code_row_words(int32_t K, int32_t bits) {
+  if (!moe::valid_bits(bits) || K <= 0 || K % 128) return 0;
+  return moe::code_row_words(K, bits);
+}

@@ -112,20 +112,22 @@ class MoELayer:
             R, K, b = cfg.rows(kind, e), cfg.cols(kind, e), int(self.bits_host[e])
             code_off.append(cw)
             sz_off.append(sw)
-            cw += ((R * K * b // 32) + 3) // 4 * 4
+            cw += (R * api.moe_code_row_words(K, b) + 3) // 4 * 4
             sw += R * (K // g)
         codes = torch.empty(max(cw, 4), dtype=torch.int32, device=dev)
         sz = torch.empty(max(sw, 1), dtype=torch.int32, device=dev)
         hdr = np.ascontiguousarray(inp.copy_headers(kind), np.int32).reshape(-1, 2)
         n_slots = hdr.shape[0]
         Kr = cfg.cols(kind, 0)
-        copy_codes = torch.empty(max(n_slots * Kr // 4, 4), dtype=torch.int32, device=dev)
+        crw = api.moe_code_row_words(Kr, 8)
+        copy_codes = torch.empty(max(n_slots * crw, 4), dtype=torch.int32, device=dev)
         copy_sz = torch.empty(max(n_slots * (Kr // g), 1), dtype=torch.int32, device=dev)
         for e in range(E + S):
             R, K, b = cfg.rows(kind, e), cfg.cols(kind, e), int(self.bits_host[e])
             w = torch.from_numpy(inp.weight(e, kind)).to(dev)
             api.moe_quant_pack(w, b, g, codes[code_off[e]:], sz[sz_off[e]:], n=R,
-                               ld_codes=K * b // 32, sz_row_stride=1, sz_group_stride=R,
+                               ld_codes=api.moe_code_row_words(K, b), sz_row_stride=1,
+                               sz_group_stride=R,
                                status=self.status)
             if e < E and n_slots:
                 sl = np.nonzero(hdr[:, 0] == e)[0]
@@ -134,8 +136,8 @@ class MoELayer:
                     if s1 - s0 != len(sl):
                         raise MoEError("copy headers must be grouped by expert")
                     rows = torch.tensor(hdr[s0:s1, 1], dtype=torch.int32, device=dev)
-                    api.moe_quant_pack(w, 8, g, copy_codes[s0 * (K // 4):],
-                                       copy_sz[s0 * (K // g):], rows=rows, ld_codes=K // 4,
+                    api.moe_quant_pack(w, 8, g, copy_codes[s0 * crw:],
+                                       copy_sz[s0 * (K // g):], rows=rows, ld_codes=crw,
                                        sz_row_stride=K // g, sz_group_stride=1,
                                        status=self.status)
             del w
@@ -217,14 +219,16 @@ class MoELayer:
         R, K, b, g = cfg.rows(kind, e), cfg.cols(kind, e), int(self.bits_host[e]), cfg.group
         o = int(kd["code_off_host"][e])
         so = int(kd["sz_off_host"][e])
-        codes = kd["codes"][o:o + R * K * b // 32].cpu().numpy().view(np.uint32).reshape(R, -1)
+        rw = api.moe_code_row_words(K, b)
+        codes = kd["codes"][o:o + R * rw].cpu().numpy().view(np.uint32).reshape(R, rw)[:, :K * b // 32]
         sz = kd["sz"][so:so + R * (K // g)].cpu().numpy().view(np.uint32).reshape(K // g, R)
         return codes, sz
 
     def packed_copies(self, kind: int):
         kd, cfg = self.kinds[kind], self.cfg
         K, g, n = cfg.cols(kind, 0), cfg.group, kd["n_slots"]
-        codes = kd["copy_codes"][:n * K // 4].cpu().numpy().view(np.uint32).reshape(n, -1)
+        rw = api.moe_code_row_words(K, 8)
+        codes = kd["copy_codes"][:n * rw].cpu().numpy().view(np.uint32).reshape(n, rw)[:, :K // 4]
         sz = kd["copy_sz"][:n * (K // g)].cpu().numpy().view(np.uint32).reshape(n, K // g)
         return codes, sz
 

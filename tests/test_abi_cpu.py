@@ -156,3 +156,13 @@ def test_switch_and_ffn_validation(lib):
     keep.append(bits)
     L.bits_host = bits.ctypes.data
     assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None) == -2
+
+
+def test_code_row_words(lib):
+    # K*bits/32 words of codes plus 16 (32 at 8 bits) words of padding
+    assert lib.moe_code_row_words(4096, 4) == 4096 * 4 // 32 + 16
+    assert lib.moe_code_row_words(4096, 8) == 4096 // 4 + 32
+    assert lib.moe_code_row_words(1408, 3) == 1408 * 3 // 32 + 16
+    assert lib.moe_code_row_words(128, 2) == 8 + 16
+    for K, b in ((4096, 5), (100, 4), (0, 4), (-128, 8)):
+        assert lib.moe_code_row_words(K, b) == 0
