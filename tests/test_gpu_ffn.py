@@ -129,3 +129,42 @@ def test_ffn_run_to_run_deterministic():
     y2 = layer.forward(x).clone()
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
+
+
+def test_mixtral_prefill_parity(orc):
+    # 4096 tokens, Zipf-skewed loads: experts with up to ~3300 rows, many
+    # 64-token tiles per expert
+    _sampled_parity(orc, "mixtral-prefill", 12)
+
+
+def test_deepseek_prefill_parity(orc):
+    # 8192 tokens, 64 routed experts + 2 shared experts over all tokens
+    _sampled_parity(orc, "deepseek-prefill", 12)
+
+
+def test_qwen_stress_mask_redraws(orc):
+    # fresh activations every step, the copy mask redrawn every 10 steps
+    wk = mi.WORKLOADS["qwen-stress"]
+    inp = mi.LayerInputs(wk.layer)
+    import paper_2503_21135_amd as P
+    layer = P.MoELayer(inp)
+    cache = {}
+    for step in (0, 10, 19):
+        epoch = step // wk.redraw_every
+        layer.set_epoch(epoch)
+        rs = oracle_row_slots(orc, inp, epoch=epoch)
+        for kd in range(3):
+            assert np.array_equal(layer.row_slot(kd), rs[kd])
+        batch = mi.make_batch(wk, inp, step=step)
+        y, b = _run(layer, batch.x, batch.bias)
+        toks = np.arange(0, wk.tokens, wk.tokens // 8)
+        key = ("epoch", epoch)
+        wc = cache.setdefault(key, {})
+        res = orc.layer_forward(inp, batch.x, bias=batch.bias, row_slot=rs, tokens=toks,
+                                weight_cache=wc)
+        routing_matches(layer, res, b)
+        err = rel_l2(y[toks], res["y"])
+        print("qwen step", step, "epoch", epoch, "switched %d%%" % inp.switch_percent(epoch),
+              "rel_l2", err, flush=True)
+        assert err <= TOL
+        assert err <= 5e-4
