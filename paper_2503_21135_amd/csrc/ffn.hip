@@ -65,6 +65,8 @@ struct FfnArgs {
   float* hsum;         // [max(f,fs)/g][rows] group sums of h rows
   float* o;
   int64_t split_stride;
+  int n_split_out;     // slices of o the combine adds (tile launches zero the others)
+  int32_t* tile_prefix;   // workspace: 4 x (MOE_MAX_EXPERTS + 1) item prefixes
   uint32_t x_bytes, h_bytes, xsum_bytes, hsum_bytes;   // resource sizes (< 2^31)
   uint32_t copy_bytes[3], copy_sz_bytes[3];
   int E, S, d, f, fs, group;
@@ -138,15 +140,17 @@ __device__ __forceinline__ void dequant_b(const uint32_t (&cw)[NW], u32x4 (&wf)[
       wf[0][m] = u32x4{pair8(ubyte_f32(w0, 0), ubyte_f32(w0, 2)), pair8(ubyte_f32(w0, 1), ubyte_f32(w0, 3)),
                        pair8(ubyte_f32(w1, 0), ubyte_f32(w1, 2)), pair8(ubyte_f32(w1, 1), ubyte_f32(w1, 3))};
     }
-  } else {  // 3-bit planes, NM == 4: words 0/1 the 2-bit plane, word 2 the 1-bit plane
+  } else {  // 3-bit: per 32-code block, words 0/1 the 2-bit plane, word 2 the 1-bit plane
+    static_assert(NM % 4 == 0, "3-bit shares are whole 32-code blocks");
 #pragma unroll
     for (int m = 0; m < NM; m++) {
+      const int blk = 3 * (m / 4);
       uint32_t lo[4], hi[4];
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        const int p = 4 * m + j;   // output register: local codes 2p, 2p+1
-        lo[j] = andor(cw[p >> 3] >> (2 * (p & 7)), 0x00030003u, vm);
-        hi[j] = andor(cw[2] >> p, 0x00010001u, vh);
+        const int p = 4 * (m % 4) + j;   // output register: block codes 2p, 2p+1
+        lo[j] = andor(cw[blk + (p >> 3)] >> (2 * (p & 7)), 0x00030003u, vm);
+        hi[j] = andor(cw[blk + 2] >> p, 0x00010001u, vh);
       }
       wf[0][m] = u32x4{lo[0], lo[1], lo[2], lo[3]};
       wf[1][m] = u32x4{hi[0], hi[1], hi[2], hi[3]};
@@ -197,7 +201,23 @@ __device__ __forceinline__ u32x4 bload4(Rsrc r, uint32_t off, uint32_t soff = 0)
 
 template <int NW>
 __device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off, uint32_t soff) {
-  if constexpr (NW == 8) {
+  if constexpr (NW == 16 || NW == 6) {
+    // four 16-byte loads, or three 8-byte loads (12-byte shares are 8-byte aligned)
+    constexpr int P = NW == 16 ? 4 : 2;
+#pragma unroll
+    for (int c = 0; c < NW / P; c++) {
+      const uint32_t o = off == kOOB ? kOOB : off + 4u * P * c;
+      if constexpr (P == 4) {
+        const u32x4 a = bload4(r, o, soff);
+#pragma unroll
+        for (int i = 0; i < 4; i++) cw[4 * c + i] = a[i];
+      } else {
+        const auto a = __builtin_amdgcn_raw_buffer_load_b64(r, o, soff, 0);
+        cw[2 * c] = a[0];
+        cw[2 * c + 1] = a[1];
+      }
+    }
+  } else if constexpr (NW == 8) {
     const u32x4 a = bload4(r, off, soff);
     const u32x4 b = bload4(r, off == kOOB ? kOOB : off + 16u, soff);
 #pragma unroll
@@ -660,6 +680,356 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
   else if constexpr (NM == 4) dispatch_class<NM, NT, NK, 3>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
 }
 
+// ------------------------------------------------------------------ tile kernel
+// For experts with many tokens (prefill, shared experts): a workgroup computes
+// a tile of kTileTok tokens x kTileRows row positions (per kind) with
+// v_mfma_f32_32x32x16_bf16 (A = 32 tokens x 16 K, B = 32 rows x 16 K; lane l
+// holds row l % 32 and tokens 8*(r/4) + 4*(l/32) + r%4 of accumulator r).
+// Wave (wt, wr) owns 32 tokens and 32 rows; lane l dequantizes the K-half
+// l/32 of each group of its row (group code 64*half + 8*s + j feeds K-step s,
+// slot j), and reads the matching activations from an LDS tile staged one
+// group ahead.  Each A fragment feeds NK MFMAs and each dequantized B
+// fragment the whole 32-token tile.
+//
+// Work items (expert, 64-row block, token tile) come from a prefix table a
+// small plan kernel builds from the routing offsets and class counts, and
+// are spread over a persistent grid so that the workgroups of one XCD
+// (hardware places workgroup b on XCD b % 8) take consecutive items.  Within
+// an expert the items run in super-tiles of kSuper row blocks x kSuper token
+// tiles, so that the workgroups one XCD runs together share both their code
+// rows and their activation rows through that XCD's L2.
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                  c, 0, 0, 0);
+}
+
+constexpr int kTileTok = 64;    // tokens per workgroup tile (2 waves x 32)
+constexpr int kTileRows = 64;   // row positions per workgroup tile and kind (2 waves x 32)
+constexpr int kXcds = 8;
+constexpr int kSuper = 8;
+
+template <int NM2>
+struct TTile {
+  static constexpr int g = NM2 * 16;
+  static constexpr int LDW = g + 8;   // 16-byte pad per token row
+  uint16_t x[2][kTileTok][LDW];
+  float xs[2][kTileTok];
+};
+
+// Experts e0 .. e0+n_e-1 of one tile launch; bits[e - e0].
+struct TileMap {
+  int e0, n_e;
+  int8_t bits[MOE_MAX_EXPERTS];
+};
+
+// Items of expert e: (row blocks over its classes) x (token tiles); the
+// exclusive prefix over the launch's experts goes to prefix[0 .. n_e].
+template <int NK>
+__global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, int32_t* __restrict__ prefix) {
+  __shared__ int cnt[MOE_MAX_EXPERTS];
+  const int i = threadIdx.x;
+  int items = 0;
+  if (i < map.n_e) {
+    const int e = map.e0 + i;
+    const int n_tok = a.offsets[e + 1] - a.offsets[e];
+    const int tiles = (n_tok + kTileTok - 1) / kTileTok;
+    int blocks = 0;
+    if (e < a.E) {
+      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) blocks += (cc[c] + kTileRows - 1) / kTileRows;
+    } else {
+      blocks = (NK == 1 ? a.d : a.fs) / kTileRows;
+    }
+    items = tiles * blocks;
+  }
+  if (i < MOE_MAX_EXPERTS) cnt[i] = items;
+  __syncthreads();
+  if (i == 0) {
+    int acc = 0;
+    for (int j = 0; j < map.n_e; j++) {
+      const int v = cnt[j];
+      prefix[j] = acc;
+      acc += v;
+    }
+    prefix[map.n_e] = acc;
+  }
+}
+
+// One lane's source of one kind: resources, {s, z} group stride and offsets.
+struct TSrc {
+  Rsrc code, sz;
+  uint32_t sz_gstride, coff, soff;
+};
+
+template <int NM2, int NK, int BG, int BU>
+struct TCodes {
+  uint32_t cg[(kWords<NM2, BG>)];
+  uint32_t cu[(kWords<NM2, BU>)];   // unused for NK = 1
+  uint32_t szw[2];
+};
+
+template <int NM2, int NK, int BG, int BU>
+__device__ __forceinline__ void tile_load(TCodes<NM2, NK, BG, BU>& st, const TSrc (&src)[2], int gi, bool gv) {
+  constexpr uint32_t gcb0 = NM2 * 16 * BG / 8, gcb1 = NM2 * 16 * BU / 8;   // code bytes per row and group
+  bload<kWords<NM2, BG>>(st.cg, src[0].code, gv ? src[0].coff : kOOB, gv ? gi * gcb0 : 0u);
+  st.szw[0] = __builtin_amdgcn_raw_buffer_load_b32(src[0].sz, gv ? src[0].soff : kOOB,
+                                                   gv ? gi * src[0].sz_gstride : 0u, 0);
+  if constexpr (NK == 2) {
+    bload<kWords<NM2, BU>>(st.cu, src[1].code, gv ? src[1].coff : kOOB, gv ? gi * gcb1 : 0u);
+    st.szw[1] = __builtin_amdgcn_raw_buffer_load_b32(src[1].sz, gv ? src[1].soff : kOOB,
+                                                     gv ? gi * src[1].sz_gstride : 0u, 0);
+  }
+}
+
+// K-step s of one kind: dequantize this lane's 8 codes and accumulate.
+template <int NM2, int B, int NW>
+__device__ __forceinline__ void tile_step(const uint32_t (&cw)[NW], int s, const u32x4& af, uint32_t vm,
+                                          uint32_t vh, f32x16& t) {
+  u32x4 wf[kPlanes<B>][NM2];
+  dequant_b<B, NM2, NW>(cw, wf, vm, vh);   // only step s survives dead-code elimination
+#pragma unroll
+  for (int pl = 0; pl < kPlanes<B>; pl++) t = mfma32(af, wf[pl][s], t);
+}
+
+template <int NM2, int NK, int BG, int BU>
+__device__ __forceinline__ void tile_body(const FfnArgs& a, TTile<NM2>& tl, int e, int cls, int pos0, int pos1,
+                                          int R, int t0, int t1) {
+  constexpr int g = NM2 * 16;
+  constexpr int PPT = kTileTok * g / 8 / 256;   // 16-byte activation pieces per thread and group
+  static_assert(PPT * 256 * 8 == kTileTok * g, "tile must split evenly over the workgroup");
+  constexpr bool down = NK == 1;
+  const int tid = threadIdx.x;
+  const int wv = tid >> 6, lane = tid & 63;
+  const int wr = wv >> 1, wt = wv & 1;
+  const int n = lane & 31, kh = lane >> 5;
+  const bool routed = e < a.E;
+  const int K = down ? (routed ? a.f : a.fs) : a.d;
+  const int G = K / g;
+  const int be = BG == BU ? BG : (cls == 1 ? BU : BG);
+  const int kind0 = down ? 2 : 0;
+  const int32_t* order = down ? a.order_dn : a.order_gu;
+  const int pos = pos0 + wr * 32 + n;
+  const bool live = pos < pos1;
+  const int row = live ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+
+  TSrc src[2];
+#pragma unroll
+  for (int kk = 0; kk < NK; kk++) {
+    const KindDev& kd = a.kd[kind0 + kk];
+    const bool copy = (cls >> kk) & 1;
+    const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
+    const uint32_t crow_bytes = 4u * static_cast<uint32_t>(code_row_words(K, 8));
+    const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
+                            : static_cast<const void*>(kd.codes + uni(kd.code_off[e]));
+    const void* sptr = copy ? static_cast<const void*>(kd.copy_sz)
+                            : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
+    const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
+    const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
+    src[kk].code = make_rsrc(cptr, cbytes);
+    src[kk].sz = make_rsrc(sptr, sbytes);
+    src[kk].sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
+    const int slot = (copy && live) ? kd.row_slot[static_cast<int64_t>(e) * R + row] : -1;
+    const uint32_t c_base = live ? row * row_bytes + kh * (g / 2) * be / 8 : kOOB;
+    const uint32_t s_base = live ? row * 4u : kOOB;
+    const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * crow_bytes + kh * (g / 2) : kOOB;
+    const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
+    src[kk].coff = copy ? c_copy : c_base;
+    src[kk].soff = copy ? s_copy : s_base;
+  }
+  const float* xsum = down ? a.hsum : a.xsum;
+  const Rsrc xr = make_rsrc(down ? a.h : a.x, down ? a.h_bytes : a.x_bytes);
+  const Rsrc xsr = make_rsrc(xsum, down ? a.hsum_bytes : a.xsum_bytes);
+  // piece q = tid + 256*i of a group: token q / (g/8), column (q % (g/8)) * 8
+  const int acol = (tid % (g / 8)) * 8;
+  uint32_t arow[PPT];
+#pragma unroll
+  for (int i = 0; i < PPT; i++) {
+    const int p = t0 + (tid + 256 * i) / (g / 8);
+    arow[i] = p < t1 ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(a.perm[p]) * K)) +
+                           2u * acol
+                     : kOOB;
+  }
+  const uint32_t xs_off = (tid < kTileTok && t0 + tid < t1) ? 4u * static_cast<uint32_t>(t0 + tid) : kOOB;
+  auto stage_x = [&](u32x4 (&v)[PPT], float& xsv, int gi) {
+    const bool gv = gi < G;
+    const uint32_t xadv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
+    const uint32_t sadv = gv ? 4u * static_cast<uint32_t>(gi * a.rows) : 0u;
+#pragma unroll
+    for (int i = 0; i < PPT; i++) v[i] = bload4(xr, gv ? arow[i] : kOOB, xadv);
+    xsv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xsr, gv ? xs_off : kOOB, sadv, 0));
+  };
+  auto write_x = [&](const u32x4 (&v)[PPT], float xsv, int buf) {
+#pragma unroll
+    for (int i = 0; i < PPT; i++)
+      *reinterpret_cast<u32x4*>(&tl.x[buf][(tid + 256 * i) / (g / 8)][acol]) = v[i];
+    if (tid < kTileTok) tl.xs[buf][tid] = xsv;
+  };
+
+  uint32_t vm = kMagic, vh = 0x44004400u;
+  asm volatile("" : "+v"(vm), "+v"(vh));
+  f32x16 acc[NK];
+#pragma unroll
+  for (int kk = 0; kk < NK; kk++) acc[kk] = f32x16{};
+  // codes of the next two groups and activations of the next group in
+  // flight (deeper prefetch measured no faster here)
+  TCodes<NM2, NK, BG, BU> st[2];
+  tile_load<NM2, NK, BG, BU>(st[0], src, 0, 0 < G);
+  tile_load<NM2, NK, BG, BU>(st[1], src, 1, 1 < G);
+  u32x4 vx[PPT];
+  float vxs;
+  stage_x(vx, vxs, 0);
+  write_x(vx, vxs, 0);
+  __syncthreads();
+  const int tok_lane0 = wt * 32 + 4 * kh;   // tile token of accumulator 0 of this lane
+
+  auto group = [&](TCodes<NM2, NK, BG, BU>& c, int buf, int gi) {
+    stage_x(vx, vxs, gi + 1);
+    if (gi < G) {   // wave-uniform
+      f32x16 t[NK];
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) t[kk] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < NM2; s++) {
+        const u32x4 af = *reinterpret_cast<const u32x4*>(&tl.x[buf][wt * 32 + n][(g / 2) * kh + 8 * s]);
+        tile_step<NM2, BG, kWords<NM2, BG>>(c.cg, s, af, vm, vh, t[0]);
+        if constexpr (NK == 2) tile_step<NM2, BU, kWords<NM2, BU>>(c.cu, s, af, vm, vh, t[1]);
+      }
+      float sc[NK], zz[NK];
+      sc[0] = fp16_bits_to_f32(c.szw[0] & 0xFFFFu);
+      zz[0] = fp16_bits_to_f32(c.szw[0] >> 16) + kOffset<BG>;
+      if constexpr (NK == 2) {
+        sc[1] = fp16_bits_to_f32(c.szw[1] & 0xFFFFu);
+        zz[1] = fp16_bits_to_f32(c.szw[1] >> 16) + kOffset<BU>;
+      }
+      f32x4 X[4];
+#pragma unroll
+      for (int q = 0; q < 4; q++) X[q] = *reinterpret_cast<const f32x4*>(&tl.xs[buf][tok_lane0 + 8 * q]);
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++)
+#pragma unroll
+        for (int r = 0; r < 16; r++)
+          acc[kk][r] = __fmaf_rn(sc[kk], __fmaf_rn(-zz[kk], X[r / 4][r % 4], t[kk][r]), acc[kk][r]);
+    }
+    tile_load<NM2, NK, BG, BU>(c, src, gi + 2, gi + 2 < G);
+    write_x(vx, vxs, buf ^ 1);
+    __syncthreads();
+  };
+  for (int gi = 0; gi < G; gi += 2) {
+    group(st[0], 0, gi);
+    group(st[1], 1, gi + 1);
+  }
+
+  // outputs: tokens t0 + tok_lane0 + 8*(r/4) + r%4, row `row`
+  if constexpr (NK == 2) {
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      const int p = t0 + tok_lane0 + 8 * (r / 4) + (r % 4);
+      if (live && p < t1) a.h[h_row(a, p) + row] = static_cast<uint16_t>(bf16_rne(silu_mul(acc[0][r], acc[1][r])));
+    }
+  } else {
+    for (int sp = 0; sp < a.n_split_out; sp++) {
+      float* out = a.o + static_cast<int64_t>(sp) * a.split_stride;
+#pragma unroll
+      for (int r = 0; r < 16; r++) {
+        const int p = t0 + tok_lane0 + 8 * (r / 4) + (r % 4);
+        if (live && p < t1) out[static_cast<int64_t>(p) * R + row] = sp == 0 ? acc[0][r] : 0.f;
+      }
+    }
+  }
+}
+
+template <int NM2, int NK, int B>
+__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, TTile<NM2>& tl, int e, int cls, int pos0,
+                                              int pos1, int R, int t0, int t1) {
+  if constexpr (NK == 1) {
+    if (cls == 0) tile_body<NM2, 1, B, B>(a, tl, e, 0, pos0, pos1, R, t0, t1);
+    else tile_body<NM2, 1, 8, 8>(a, tl, e, 1, pos0, pos1, R, t0, t1);
+  } else {
+    if (cls == 0) tile_body<NM2, 2, B, B>(a, tl, e, 0, pos0, pos1, R, t0, t1);
+    else if (cls == 1) tile_body<NM2, 2, 8, B>(a, tl, e, 1, pos0, pos1, R, t0, t1);
+    else if (cls == 2) tile_body<NM2, 2, B, 8>(a, tl, e, 2, pos0, pos1, R, t0, t1);
+    else tile_body<NM2, 2, 8, 8>(a, tl, e, 3, pos0, pos1, R, t0, t1);
+  }
+}
+
+template <int NM2, int NK>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
+  __shared__ __attribute__((aligned(16))) TTile<NM2> tl;
+  __shared__ int pre[MOE_MAX_EXPERTS + 1];
+  for (int i = threadIdx.x; i <= map.n_e; i += blockDim.x) pre[i] = prefix[i];
+  __syncthreads();
+  const int total = pre[map.n_e];
+  const int G = gridDim.x;   // a multiple of kXcds
+  const int per = G / kXcds;
+  const int xcd = blockIdx.x % kXcds, loc = blockIdx.x / kXcds;
+  for (int it = 0;; it++) {
+    const int item = it * G + xcd * per + loc;
+    if (item >= total) break;
+    int lo = 0, hi = map.n_e - 1;   // last expert whose prefix is <= item
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (pre[mid] <= item) lo = mid; else hi = mid - 1;
+    }
+    const int e = map.e0 + lo;
+    const int local = item - pre[lo];
+    const int seg0 = uni(a.offsets[e]), seg1 = uni(a.offsets[e + 1]);
+    const int tiles = (seg1 - seg0 + kTileTok - 1) / kTileTok;
+    const bool routed = e < a.E;
+    const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
+    // (row block, token tile) of the local index: super-rows of kSuper row
+    // blocks, token tiles outer and row blocks inner within a super-row
+    int n_rb = 0;
+    if (routed) {
+      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) n_rb += (uni(cc[c]) + kTileRows - 1) / kTileRows;
+    } else {
+      n_rb = R / kTileRows;
+    }
+    const int full = (n_rb / kSuper) * kSuper * tiles;
+    int rb, tt;
+    if (local < full) {
+      const int sr = local / (kSuper * tiles), rem = local - sr * kSuper * tiles;
+      tt = rem / kSuper;
+      rb = sr * kSuper + rem % kSuper;
+    } else {
+      const int h = n_rb % kSuper, rem = local - full;
+      tt = rem / h;
+      rb = (n_rb / kSuper) * kSuper + rem % h;
+    }
+    int cls = 0, start = 0, count = R;
+    if (routed) {
+      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) {
+        const int cn = uni(cc[c]);
+        const int nb = (cn + kTileRows - 1) / kTileRows;
+        if (rb < nb) {
+          cls = c;
+          count = cn;
+          break;
+        }
+        rb -= nb;
+        start += cn;
+      }
+    }
+    const int pos0 = start + rb * kTileRows;
+    const int pos1 = min(pos0 + kTileRows, start + count);
+    const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
+    const int B = map.bits[e - map.e0];
+    if (B == 8) tile_dispatch<NM2, NK, 8>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if constexpr (NM2 % 4 == 0) tile_dispatch<NM2, NK, 3>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    __syncthreads();   // the LDS tile is reused by the next item
+  }
+}
+
 // ------------------------------------------------------------------ group sums
 // out[j * rows + p] = sum over group j of the bf16 row of permuted row p, in
 // fp32: each of g/8 lanes adds its 8 values in order, then an xor tree over
@@ -701,14 +1071,16 @@ size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 struct Plan {
   int n_split;
-  int nt_routed, nt_shared;
-  size_t xsum_bytes, h_bytes, hsum_bytes, total;
+  int nt_routed, nt_shared;   // token tiles of the streaming kernel, 0: tile kernel
+  size_t xsum_bytes, h_bytes, hsum_bytes, tile_bytes, total;
 };
 
+// Streaming kernel for up to 28 expected tokens per expert (one or two
+// 16-token MFMA tiles, weights streamed once), tile kernel beyond.
 int pick_nt(double tokens) {
   if (tokens <= 12.0) return 1;
   if (tokens <= 28.0) return 2;
-  return 4;
+  return 0;
 }
 
 Plan make_plan(const moe_layer_t* L, int T, int k) {
@@ -723,14 +1095,17 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   int ns = static_cast<int>(cdiv(4096, std::max<int64_t>(base_waves, 1)));
   ns = std::min(ns, 8);
   ns = std::min(ns, std::max(1, gmin / 8));
-  p.n_split = std::max(ns, 1);
   p.nt_routed = pick_nt(static_cast<double>(Tk) / E);
   p.nt_shared = pick_nt(static_cast<double>(T));
+  // split-K slices of the down projection only where the routed experts
+  // stream (few tokens, too few output rows to fill the machine)
+  p.n_split = p.nt_routed == 0 ? 1 : std::max(ns, 1);
   const int64_t hcols = Tk * L->d_ff + static_cast<int64_t>(S) * T * L->d_ff_shared;
   p.xsum_bytes = align256(sizeof(float) * static_cast<size_t>(rows) * (L->d_model / g));
   p.h_bytes = align256(sizeof(uint16_t) * static_cast<size_t>(hcols));
   p.hsum_bytes = align256(sizeof(float) * static_cast<size_t>(rows) * (fmax / g));
-  p.total = p.xsum_bytes + p.h_bytes + p.hsum_bytes + 256;
+  p.tile_bytes = align256(sizeof(int32_t) * 4 * (MOE_MAX_EXPERTS + 1));
+  p.total = p.xsum_bytes + p.h_bytes + p.hsum_bytes + p.tile_bytes + 256;
   return p;
 }
 
@@ -819,6 +1194,28 @@ WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
   return m;
 }
 
+TileMap tile_map(const moe_layer_t* L, bool shared) {
+  TileMap m{};
+  m.e0 = shared ? L->n_experts : 0;
+  m.n_e = shared ? L->n_shared : L->n_experts;
+  for (int i = 0; i < m.n_e; i++) m.bits[i] = static_cast<int8_t>(L->bits_host[m.e0 + i]);
+  return m;
+}
+
+// Persistent tile grid: two workgroups per compute unit, a multiple of the
+// XCD count.
+int tile_grid() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
+    cached[dev] = std::max(kXcds, (2 * cu) / kXcds * kXcds);
+  }
+  return cached[dev];
+}
+
 inline void mark(hipEvent_t* ev, int n_ev, int i, hipStream_t s) {
   if (ev && i < n_ev && ev[i]) (void)hipEventRecord(ev[i], s);
 }
@@ -842,13 +1239,28 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     if (n_wg == 0) return;
     const dim3 grid(static_cast<unsigned>(n_wg * nsplit));
     if (nt == 1) hipLaunchKernelGGL((ffn_stream_kernel<NM, 1, NK>), grid, dim3(256), 0, s, a, m, nsplit);
-    else if (nt == 2) hipLaunchKernelGGL((ffn_stream_kernel<NM, 2, NK>), grid, dim3(256), 0, s, a, m, nsplit);
-    else hipLaunchKernelGGL((ffn_stream_kernel<NM, 4, NK>), grid, dim3(256), 0, s, a, m, nsplit);
+    else hipLaunchKernelGGL((ffn_stream_kernel<NM, 2, NK>), grid, dim3(256), 0, s, a, m, nsplit);
+  };
+  int32_t* prefix = a.tile_prefix;
+  auto tile = [&](auto nk, bool shared) {
+    constexpr int NK = decltype(nk)::value;
+    const TileMap m = tile_map(L, shared);
+    int32_t* pf = prefix;
+    prefix += MOE_MAX_EXPERTS + 1;
+    if (m.n_e == 0) return;
+    hipLaunchKernelGGL((tile_plan_kernel<NK>), dim3(1), dim3(256), 0, s, a, m, pf);
+    hipLaunchKernelGGL((ffn_tile_kernel<2 * NM, NK>), dim3(static_cast<unsigned>(tile_grid())), dim3(256), 0, s,
+                       a, m, static_cast<const int32_t*>(pf));
+  };
+  auto run = [&](auto nk, bool shared, int nt, int nsplit) {
+    const WgMap m = stream_map(L, shared, decltype(nk)::value == 1);
+    if (nt == 0) tile(nk, shared);
+    else stream(nk, m, nt, nsplit);
   };
   using two = std::integral_constant<int, 2>;
   using one = std::integral_constant<int, 1>;
-  stream(two{}, stream_map(L, false, false), p.nt_routed, 1);
-  if (S > 0) stream(two{}, stream_map(L, true, false), p.nt_shared, 1);
+  run(two{}, false, p.nt_routed, 1);
+  if (S > 0) run(two{}, true, p.nt_shared, 1);
   mark(ev, n_ev, 2, s);
   {  // group sums of h, [max(f,fs)/g][rows]
     const int64_t n = static_cast<int64_t>(a.Tk) * (a.f / g) * (g / 8);
@@ -864,8 +1276,8 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     }
   }
   mark(ev, n_ev, 3, s);
-  stream(one{}, stream_map(L, false, true), p.nt_routed, p.n_split);
-  if (S > 0) stream(one{}, stream_map(L, true, true), p.nt_shared, p.n_split);
+  run(one{}, false, p.nt_routed, p.n_split);
+  if (S > 0) run(one{}, true, p.nt_shared, p.n_split);
   mark(ev, n_ev, 4, s);
 }
 
@@ -928,6 +1340,8 @@ int ffn_entry(const moe_layer_t* L, const uint16_t* x, int32_t T, int32_t k,
   a.xsum = reinterpret_cast<float*>(w);
   a.h = reinterpret_cast<uint16_t*>(w + p.xsum_bytes);
   a.hsum = reinterpret_cast<float*>(w + p.xsum_bytes + p.h_bytes);
+  a.tile_prefix = reinterpret_cast<int32_t*>(w + p.xsum_bytes + p.h_bytes + p.hsum_bytes);
+  a.n_split_out = p.n_split;
   a.o = o;
   a.split_stride = static_cast<int64_t>(T) * (k + L->n_shared) * L->d_model;
   {  // sizes of the buffer resources; every one must stay below 2^31 bytes
