@@ -278,14 +278,19 @@ int moe_expert_ffn_mixed(const moe_layer_t* L, const uint16_t* x, int32_t T,
 
 /*
  * moe_expert_ffn_mixed_ev -- moe_expert_ffn_mixed that also records HIP
- * events on `stream` at its stage boundaries, so a caller can time each
- * kernel of the FFN on the stream it runs on.  Not on the hot path of a
- * production caller; same arguments, results and errors otherwise.
+ * events on `stream`, so a caller can time the FFN's stages on the stream
+ * they run on.  The events are attached to the kernel dispatches themselves
+ * (they take the dispatch's begin or end timestamp; no marker packets are
+ * added between kernels).  Not on the hot path of a production caller; same
+ * arguments, results and errors otherwise.
  *   events    host array of n_events hipEvent_t handles (as void*), each
  *             created by the caller; NULL entries are skipped:
- *             [0] before the first launch, [1] after the activation group
- *             sums, [2] after the gate/up kernels, [3] after the hidden-
- *             activation group sums, [4] after the down kernels.
+ *             [0] begin of the activation group-sum launch,
+ *             [1] begin of the first gate/up launch,
+ *             [2] end of the last gate/up launch,
+ *             [3] begin of the first down launch,
+ *             [4] end of the last down launch.
+ *             A stage with no launch records its events as stream markers.
  */
 int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
                             int32_t k, const int32_t* offsets,

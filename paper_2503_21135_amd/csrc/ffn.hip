@@ -30,8 +30,11 @@
 //     B = weights (rows) leaves each lane the results of its own row r16 for
 //     tokens 4*kq .. 4*kq+3, so the lane applies its own row's scale/zero.
 #include <algorithm>
+#include <functional>
 #include <type_traits>
 #include <vector>
+
+#include <hip/hip_ext.h>
 
 #include "common.hpp"
 
@@ -1216,8 +1219,27 @@ int tile_grid() {
   return cached[dev];
 }
 
-inline void mark(hipEvent_t* ev, int n_ev, int i, hipStream_t s) {
-  if (ev && i < n_ev && ev[i]) (void)hipEventRecord(ev[i], s);
+// One kernel launch of a stage; `start` / `stop` (may be null) are HIP events
+// that take the dispatch's own begin / end timestamps.
+using Launch = std::function<void(hipEvent_t start, hipEvent_t stop)>;
+
+template <typename F, typename... A>
+void klaunch(F kernel, dim3 grid, dim3 block, hipStream_t s, hipEvent_t start, hipEvent_t stop,
+             A... args) {
+  if (start || stop) hipExtLaunchKernelGGL(kernel, grid, block, 0, s, start, stop, 0, args...);
+  else hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
+
+// Issues a stage's launches in order: the first carries `start`, the last
+// `stop`.  An empty stage records the events as plain stream markers.
+void issue(const std::vector<Launch>& v, hipEvent_t start, hipEvent_t stop, hipStream_t s) {
+  if (v.empty()) {
+    if (start) (void)hipEventRecord(start, s);
+    if (stop) (void)hipEventRecord(stop, s);
+    return;
+  }
+  for (size_t i = 0; i < v.size(); i++)
+    v[i](i == 0 ? start : nullptr, i + 1 == v.size() ? stop : nullptr);
 }
 
 template <int NM>
@@ -1225,60 +1247,68 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
                 hipEvent_t* ev, int n_ev) {
   constexpr int g = NM * 32;
   const int S = a.S;
-  mark(ev, n_ev, 0, s);
+  auto event = [&](int i) -> hipEvent_t { return (ev && i < n_ev) ? ev[i] : nullptr; };
+  std::vector<Launch> xsum, gate_up, hsum, down;
   {  // group sums of the gathered activations, [d/g][rows]
     const int64_t n = static_cast<int64_t>(a.rows) * (a.d / g) * (g / 8);
-    hipLaunchKernelGGL(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0,
-                       s, a, a.x, a.perm, static_cast<int64_t>(a.d), 0, a.rows, a.d,
-                       const_cast<float*>(a.xsum));
+    xsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+      klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
+              a, a.x, a.perm, static_cast<int64_t>(a.d), 0, a.rows, a.d, const_cast<float*>(a.xsum));
+    });
   }
-  mark(ev, n_ev, 1, s);
-  auto stream = [&](auto nk, const WgMap& m, int nt, int nsplit) {
+  int32_t* prefix = a.tile_prefix;
+  auto add = [&](std::vector<Launch>& v, auto nk, bool shared, int nt, int nsplit) {
     constexpr int NK = decltype(nk)::value;
+    if (nt == 0) {  // tile path: plan kernel, then the persistent tile kernel
+      const TileMap m = tile_map(L, shared);
+      const int32_t* pf = prefix;
+      prefix += MOE_MAX_EXPERTS + 1;
+      if (m.n_e == 0) return;
+      v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(tile_plan_kernel<NK>, dim3(1), dim3(256), s, e0, e1, a, m, const_cast<int32_t*>(pf));
+      });
+      v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(ffn_tile_kernel<2 * NM, NK>, dim3(static_cast<unsigned>(tile_grid())), dim3(256), s,
+                e0, e1, a, m, pf);
+      });
+      return;
+    }
+    const WgMap m = stream_map(L, shared, NK == 1);
     const int64_t n_wg = static_cast<int64_t>(m.n_e) * (m.n_sw + m.per_e);
     if (n_wg == 0) return;
     const dim3 grid(static_cast<unsigned>(n_wg * nsplit));
-    if (nt == 1) hipLaunchKernelGGL((ffn_stream_kernel<NM, 1, NK>), grid, dim3(256), 0, s, a, m, nsplit);
-    else hipLaunchKernelGGL((ffn_stream_kernel<NM, 2, NK>), grid, dim3(256), 0, s, a, m, nsplit);
-  };
-  int32_t* prefix = a.tile_prefix;
-  auto tile = [&](auto nk, bool shared) {
-    constexpr int NK = decltype(nk)::value;
-    const TileMap m = tile_map(L, shared);
-    int32_t* pf = prefix;
-    prefix += MOE_MAX_EXPERTS + 1;
-    if (m.n_e == 0) return;
-    hipLaunchKernelGGL((tile_plan_kernel<NK>), dim3(1), dim3(256), 0, s, a, m, pf);
-    hipLaunchKernelGGL((ffn_tile_kernel<2 * NM, NK>), dim3(static_cast<unsigned>(tile_grid())), dim3(256), 0, s,
-                       a, m, static_cast<const int32_t*>(pf));
-  };
-  auto run = [&](auto nk, bool shared, int nt, int nsplit) {
-    const WgMap m = stream_map(L, shared, decltype(nk)::value == 1);
-    if (nt == 0) tile(nk, shared);
-    else stream(nk, m, nt, nsplit);
+    v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, dim3(256), s, e0, e1, a, m, nsplit);
+      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, dim3(256), s, e0, e1, a, m, nsplit);
+    });
   };
   using two = std::integral_constant<int, 2>;
   using one = std::integral_constant<int, 1>;
-  run(two{}, false, p.nt_routed, 1);
-  if (S > 0) run(two{}, true, p.nt_shared, 1);
-  mark(ev, n_ev, 2, s);
+  add(gate_up, two{}, false, p.nt_routed, 1);
+  if (S > 0) add(gate_up, two{}, true, p.nt_shared, 1);
   {  // group sums of h, [max(f,fs)/g][rows]
     const int64_t n = static_cast<int64_t>(a.Tk) * (a.f / g) * (g / 8);
     if (n > 0)
-      hipLaunchKernelGGL(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256),
-                         0, s, a, a.h, static_cast<const int32_t*>(nullptr), int64_t{0}, 0, a.Tk,
-                         a.f, a.hsum);
+      hsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
+                a, static_cast<const uint16_t*>(a.h), static_cast<const int32_t*>(nullptr),
+                int64_t{0}, 0, a.Tk, a.f, a.hsum);
+      });
     if (S > 0) {
       const int64_t n2 = static_cast<int64_t>(a.rows - a.Tk) * (a.fs / g) * (g / 8);
-      hipLaunchKernelGGL(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n2, 256))), dim3(256),
-                         0, s, a, a.h, static_cast<const int32_t*>(nullptr), int64_t{0}, a.Tk, a.rows,
-                         a.fs, a.hsum);
+      hsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n2, 256))), dim3(256), s, e0,
+                e1, a, static_cast<const uint16_t*>(a.h), static_cast<const int32_t*>(nullptr),
+                int64_t{0}, a.Tk, a.rows, a.fs, a.hsum);
+      });
     }
   }
-  mark(ev, n_ev, 3, s);
-  run(one{}, false, p.nt_routed, p.n_split);
-  if (S > 0) run(one{}, true, p.nt_shared, p.n_split);
-  mark(ev, n_ev, 4, s);
+  add(down, one{}, false, p.nt_routed, p.n_split);
+  if (S > 0) add(down, one{}, true, p.nt_shared, p.n_split);
+  issue(xsum, event(0), nullptr, s);
+  issue(gate_up, event(1), event(2), s);
+  issue(hsum, nullptr, nullptr, s);
+  issue(down, event(3), event(4), s);
 }
 
 }  // namespace

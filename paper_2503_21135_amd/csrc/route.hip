@@ -50,32 +50,83 @@ __device__ __forceinline__ float tree_sum(float v) {
   return __shfl(v, 0, kWave);
 }
 
-constexpr int kMaxD = 8192;   // d_model limit of the router (x row staged in LDS)
+constexpr int kMaxD = 8192;     // d_model limit of the router
+constexpr int kRouteWaves = 8;  // waves per router workgroup
 
-// One workgroup (4 waves) per token.  The token's activations are staged in
-// LDS as fp32; wave w computes the logits of experts w, w+4, ... with the
-// header's fixed order; wave 0 then selects the top k and forms the weights.
-__global__ void __launch_bounds__(256)
+// Partial dot products of NE router rows (experts e0, e0 + es, ...) with the
+// token row: lane l accumulates columns l, l + 64, l + 128, ... in ascending
+// order with one fused multiply-add each, the header's per-lane order.  The
+// activations are read straight from global memory (bf16 -> fp32 is exact),
+// and each batch issues RB columns of every row before the first FMA so the
+// whole batch is in flight at once.
+template <int NE, int RB>
+__device__ __forceinline__ void router_partials(const uint16_t* __restrict__ xr,
+                                                const float* __restrict__ wr, int d, int e0,
+                                                int es, int lane, float (&acc)[NE]) {
+#pragma unroll
+  for (int j = 0; j < NE; j++) acc[j] = 0.0f;
+  int c0 = 0;
+  for (; c0 + kWave * RB <= d; c0 += kWave * RB) {
+    uint32_t xb[RB];
+    float w[NE][RB];
+#pragma unroll
+    for (int i = 0; i < RB; i++) {
+      const int c = c0 + kWave * i + lane;
+      xb[i] = xr[c];
+#pragma unroll
+      for (int j = 0; j < NE; j++) w[j][i] = wr[static_cast<int64_t>(e0 + j * es) * d + c];
+    }
+#pragma unroll
+    for (int i = 0; i < RB; i++) {
+      const float xv = __uint_as_float(xb[i] << 16);
+#pragma unroll
+      for (int j = 0; j < NE; j++) acc[j] = __fmaf_rn(xv, w[j][i], acc[j]);
+    }
+  }
+  for (int c = c0 + lane; c < d; c += kWave) {  // tail: fewer than RB columns per lane
+    const float xv = __uint_as_float(static_cast<uint32_t>(xr[c]) << 16);
+#pragma unroll
+    for (int j = 0; j < NE; j++)
+      acc[j] = __fmaf_rn(xv, wr[static_cast<int64_t>(e0 + j * es) * d + c], acc[j]);
+  }
+}
+
+// One workgroup (8 waves) per token.  Wave w owns experts w, w + 8, ... and
+// computes their logits four, two or one at a time; wave 0 then selects the
+// top k and forms the weights.
+__global__ void __launch_bounds__(kRouteWaves * kWave)
 route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
                   const float* __restrict__ bias, int E, int k,
                   int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
-  __shared__ float xs[kMaxD];
   __shared__ float lgs[MOE_MAX_EXPERTS];
   const int t = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const uint16_t* xr = x + static_cast<int64_t>(t) * d;
-  for (int c = threadIdx.x; c < d; c += blockDim.x)
-    xs[c] = __uint_as_float(static_cast<uint32_t>(xr[c]) << 16);
-  __syncthreads();
-  for (int e = wv; e < E; e += 4) {
-    const float* we = wr + static_cast<int64_t>(e) * d;
-    float acc = 0.0f;
-#pragma unroll 8
-    for (int c = lane; c < d; c += kWave) acc = __fmaf_rn(xs[c], we[c], acc);
+  const int mine = wv < E ? (E - 1 - wv) / kRouteWaves + 1 : 0;  // experts of this wave
+  auto finish = [&](int e, float acc) {
     float v = tree_sum(acc);
     if (bias) v = v + bias[e];
     if (lane == 0) lgs[e] = v;
+  };
+  int m = 0;
+  for (; m + 4 <= mine; m += 4) {
+    float acc[4];
+    router_partials<4, 32>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
+#pragma unroll
+    for (int j = 0; j < 4; j++) finish(wv + (m + j) * kRouteWaves, acc[j]);
+  }
+  if (m + 2 <= mine) {
+    float acc[2];
+    router_partials<2, 32>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
+#pragma unroll
+    for (int j = 0; j < 2; j++) finish(wv + (m + j) * kRouteWaves, acc[j]);
+    m += 2;
+  }
+  if (m < mine) {
+    float acc[1];
+    router_partials<1, 64>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
+    finish(wv + m * kRouteWaves, acc[0]);
   }
   __syncthreads();
   if (wv != 0) return;
@@ -216,6 +267,105 @@ route_scatter_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k, 
   }
 }
 
+constexpr int kPermWaves = 16;   // waves of the fused permutation workgroup
+constexpr int kFusedChunks = 16; // token chunks the fused path holds in LDS
+
+// Histogram, scans and stable scatter of up to kFusedChunks chunks in one
+// workgroup (batches of up to 1024 tokens).  The segment order is the same as
+// the three-kernel path's: experts ascending, then tokens ascending, shared
+// experts last.
+__global__ void __launch_bounds__(kPermWaves * kWave)
+route_permute_fused_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k, int S,
+                           int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token,
+                           int32_t* __restrict__ inv_perm) {
+  __shared__ int32_t cb[kFusedChunks * MOE_MAX_EXPERTS];  // chunk counts, then chunk bases
+  __shared__ int32_t seg[MOE_MAX_EXPERTS + 1];            // segment offsets, then the total
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int n_chunks = (T + kChunk - 1) / kChunk;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // wave c holds chunk c (n_chunks <= kPermWaves) and keeps its choices
+  const int c = wv;
+  const int t = c * kChunk + lane;
+  const bool live = t < T;
+  int mine[MOE_MAX_TOPK];
+  for (int j = 0; j < k; j++) mine[j] = live ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
+  if (c < n_chunks) {
+    for (int e = 0; e < E; e++) {
+      bool has = false;
+      for (int j = 0; j < k; j++) has |= (mine[j] == e);
+      const uint64_t m = __ballot(has);
+      if (lane == 0) cb[c * E + e] = __popcll(m);
+    }
+  }
+  __syncthreads();
+  // per expert: exclusive scan over the chunks
+  if (threadIdx.x < E) {
+    const int e = threadIdx.x;
+    int run = 0;
+    for (int cc = 0; cc < n_chunks; cc++) {
+      const int v = cb[cc * E + e];
+      cb[cc * E + e] = run;
+      run += v;
+    }
+    seg[e] = run;
+  }
+  __syncthreads();
+  // exclusive scan of the segment sizes over experts: four per lane of wave 0
+  if (wv == 0) {
+    int v[4];
+    int sum = 0;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int e = 4 * lane + i;
+      v[i] = e < E ? seg[e] : 0;
+      sum += v[i];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += o;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int e = 4 * lane + i;
+      if (e < E) seg[e] = run;
+      run += v[i];
+    }
+    if (lane == kWave - 1) seg[MOE_MAX_EXPERTS] = incl;
+  }
+  __syncthreads();
+  const int routed = seg[MOE_MAX_EXPERTS];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) offsets[e] = seg[e];
+  for (int s2 = threadIdx.x; s2 <= S; s2 += blockDim.x) offsets[E + s2] = routed + s2 * T;
+  if (c >= n_chunks) return;
+  int pos[MOE_MAX_TOPK];
+  for (int j = 0; j < k; j++) pos[j] = -1;
+  for (int e = 0; e < E; e++) {
+    bool has = false;
+    for (int j = 0; j < k; j++) has |= (mine[j] == e);
+    const uint64_t m = __ballot(has);
+    if (has) {
+      const int p = seg[e] + cb[c * E + e] + __popcll(m & below);
+      for (int j = 0; j < k; j++)
+        if (mine[j] == e) pos[j] = p;
+    }
+  }
+  if (!live) return;
+  const int64_t row = static_cast<int64_t>(t) * (k + S);
+  for (int j = 0; j < k; j++) {
+    perm_token[pos[j]] = t;
+    inv_perm[row + j] = pos[j];
+  }
+  for (int s2 = 0; s2 < S; s2++) {
+    const int p = routed + s2 * T + t;
+    perm_token[p] = t;
+    inv_perm[row + k + s2] = p;
+  }
+}
+
 // x_perm[p] = x[perm_token[p]] (16-byte copies; d % 8 == 0).
 __global__ void __launch_bounds__(256)
 gather_rows_kernel(const uint16_t* __restrict__ x, int d, const int32_t* __restrict__ perm_token,
@@ -260,16 +410,20 @@ extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const 
   const int n_chunks = static_cast<int>(cdiv(T, kChunk));
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + need / 2);
-  if (T > 0) {
-    hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(T)), dim3(256), 0, s,
-                       x, T, d, w_router, bias, E, k, topk_ids, topk_w);
+  if (T > 0)
+    hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(T)), dim3(kRouteWaves * kWave),
+                       0, s, x, T, d, w_router, bias, E, k, topk_ids, topk_w);
+  if (n_chunks <= kFusedChunks) {
+    hipLaunchKernelGGL(route_permute_fused_kernel, dim3(1), dim3(kPermWaves * kWave), 0, s,
+                       topk_ids, T, E, k, S, offsets, perm_token, inv_perm);
+  } else {
     hipLaunchKernelGGL(route_hist_kernel, dim3(n_chunks), dim3(64), 0, s, topk_ids, T, E, k, hist);
-  }
-  hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(256), 0, s, hist, n_chunks, T, E, k, S,
-                     base, offsets);
-  if (T > 0) {
+    hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(256), 0, s, hist, n_chunks, T, E, k, S,
+                       base, offsets);
     hipLaunchKernelGGL(route_scatter_kernel, dim3(n_chunks), dim3(64), 0, s, topk_ids, T, E, k, S,
                        base, offsets, perm_token, inv_perm);
+  }
+  if (T > 0) {
     if (x_perm) {
       const int64_t rows = static_cast<int64_t>(T) * (k + S);
       const int64_t n = rows * (d / 8);

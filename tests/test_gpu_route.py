@@ -63,7 +63,8 @@ def test_route_workloads(orc, name):
 
 
 @pytest.mark.parametrize("T,E,k,S,d", [(1, 8, 2, 0, 256), (65, 8, 8, 0, 256), (130, 64, 6, 2, 128),
-                                       (7, 256, 16, 0, 64), (200, 3, 1, 1, 192)])
+                                       (7, 256, 16, 0, 64), (200, 3, 1, 1, 192),
+                                       (1024, 255, 16, 1, 64), (1025, 60, 4, 1, 128)])
 def test_route_edges(orc, T, E, k, S, d):
     rng = np.random.default_rng(T + E)
     x = mi.bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
