@@ -70,7 +70,8 @@ struct FfnArgs {
   int64_t split_stride;
   int n_split_out;     // slices of o the combine adds (tile launches zero the others)
   int32_t* tile_prefix;   // workspace: 4 x (MOE_MAX_EXPERTS + 1) item prefixes
-  uint32_t x_bytes, h_bytes, xsum_bytes, hsum_bytes;   // resource sizes (< 2^31)
+  const uint16_t* x16;  // [rows][d] fp16 copies of the gathered x rows (tile kernel)
+  uint32_t x_bytes, h_bytes, xsum_bytes, hsum_bytes, x16_bytes;   // resource sizes (< 2^31)
   uint32_t copy_bytes[3], copy_sz_bytes[3];
   int E, S, d, f, fs, group;
   int Tk;    // routed rows T*k
@@ -241,6 +242,17 @@ __device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off, 
   } else {
     cw[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, soff, 0);
   }
+}
+
+// Vector-memory instructions bload<NW> issues.
+template <int NW>
+constexpr int kCodeLoads = NW == 16 ? 4 : (NW == 6 ? 3 : (NW == 8 ? 2 : 1));
+
+// Direct-to-LDS load of 16 bytes per lane: lane l of the wave writes
+// lds + 16*l (lds wave-uniform); a lane whose offset lies past the resource
+// writes zeros.
+__device__ __forceinline__ void lds_dma16(Rsrc r, void* lds, uint32_t off, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, soff, 0, 0);
 }
 
 // ------------------------------------------------------------------ streaming kernel
@@ -684,42 +696,62 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
 }
 
 // ------------------------------------------------------------------ tile kernel
-// For experts with many tokens (prefill, shared experts): a workgroup computes
-// a tile of kTileTok tokens x kTileRows row positions (per kind) with
-// v_mfma_f32_32x32x16_bf16 (A = 32 tokens x 16 K, B = 32 rows x 16 K; lane l
-// holds row l % 32 and tokens 8*(r/4) + 4*(l/32) + r%4 of accumulator r).
-// Wave (wt, wr) owns 32 tokens and 32 rows; lane l dequantizes the K-half
-// l/32 of each group of its row (group code 64*half + 8*s + j feeds K-step s,
-// slot j), and reads the matching activations from an LDS tile staged one
-// group ahead.  Each A fragment feeds NK MFMAs and each dequantized B
-// fragment the whole 32-token tile.
+// For experts with many tokens (prefill, shared experts), where the
+// contraction is MFMA-bound: a workgroup computes a tile of kTileTok tokens x
+// kTileRows row positions (per kind) with v_mfma_f32_32x32x16_f16.  This is
+// the paper's formulation of the dequantized product (Sec. V-B: dequantize to
+// a 16-bit operand, then matrix-core multiply): the weight operand is
+// fp16(s * (q - z)) -- one rounding per weight -- and the activations enter
+// as fp16 (the bf16 activations and hidden values convert exactly while
+// their magnitude stays below 65504).  The scale is thus inside the operand
+// and the accumulation runs over the whole K with no per-group epilogue.
 //
-// Work items (expert, 64-row block, token tile) come from a prefix table a
-// small plan kernel builds from the routing offsets and class counts, and
-// are spread over a persistent grid so that the workgroups of one XCD
-// (hardware places workgroup b on XCD b % 8) take consecutive items.  Within
-// an expert the items run in super-tiles of kSuper row blocks x kSuper token
-// tiles, so that the workgroups one XCD runs together share both their code
-// rows and their activation rows through that XCD's L2.
+// Dequantization: a code q OR-ed into the mantissa of fp16 1024.0 gives
+// exactly 1024 + q (q < 1024); one packed fp16 subtraction of 1024 + z makes
+// q - z exactly, one packed fp16 multiplication by s rounds the product.
+//
+// Wave w owns rows [32w, 32w + 32) of the tile and all kTileTok tokens (four
+// 32-token blocks): every dequantized B fragment feeds four MFMAs per kind,
+// and every A fragment (from LDS) NK.  Lane l holds row l % 32 and the K-half
+// l/32 of each group (group code g/2*half + 8*s + j feeds K-step s, slot j);
+// accumulator element r of lane l is token 8*(r/4) + 4*(l/32) + r%4 of the
+// block.  The activations of one group for the whole tile are staged in LDS
+// by direct-to-LDS loads, double-buffered, with the XOR swizzle of the
+// streaming kernel; the packed codes of the next group are in flight in
+// registers.
+//
+// Work items (expert, row block, token tile) come from a prefix table a small
+// plan kernel builds from the routing offsets and class counts, and are
+// spread over a persistent grid so that the workgroups of one XCD (hardware
+// places workgroup b on XCD b % 8) take consecutive items.  Within an expert
+// the items run in super-tiles of kSuper row blocks x kSuper token tiles, so
+// that the workgroups one XCD runs together share both their code rows and
+// their activation rows through that XCD's L2.
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
-                                                  c, 0, 0, 0);
+__device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                 0, 0);
 }
 
-constexpr int kTileTok = 64;    // tokens per workgroup tile (2 waves x 32)
-constexpr int kTileRows = 64;   // row positions per workgroup tile and kind (2 waves x 32)
+constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token blocks)
+constexpr int kTileRows = 128;  // row positions per workgroup tile and kind (4 waves x 32)
 constexpr int kXcds = 8;
 constexpr int kSuper = 8;
+constexpr uint32_t kMagic16 = 0x64006400u;   // two fp16 1024.0
 
+// LDS of the tile kernel: two stages of kTileTok token rows x g columns of
+// fp16 activations in 16-byte slots (slot s: token s / (g/8), column chunk
+// (s % (g/8)) ^ (token % (g/8))).
 template <int NM2>
-struct TTile {
+struct HTile {
   static constexpr int g = NM2 * 16;
-  static constexpr int LDW = g + 8;   // 16-byte pad per token row
-  uint16_t x[2][kTileTok][LDW];
-  float xs[2][kTileTok];
+  static constexpr int SPT = g / 8;
+  static constexpr int SLOTS = kTileTok * SPT;
+  u32x4 a[2][SLOTS];
 };
 
 // Experts e0 .. e0+n_e-1 of one tile launch; bits[e - e0].
@@ -767,46 +799,105 @@ struct TSrc {
   uint32_t sz_gstride, coff, soff;
 };
 
+// Packed-code words of one lane's half of a group (g/2 codes).
+template <int NM2, int B>
+constexpr int kHalfWords = NM2 * 16 / 2 * B / 32;
+
+// fp16 pair (1024 + q_lo, 1024 + q_hi) from two codes at bit offset sh of
+// each half-word (b <= 8 bits wide, masked by m).
+__device__ __forceinline__ uint32_t unpack16(uint32_t w, int sh, uint32_t m, uint32_t vm) {
+  return ((w >> sh) & m) | vm;
+}
+
+// B fragment of K-step s: 8 fp16 weights s*(q - z) of this lane's row.
+template <int NM2, int B>
+__device__ __forceinline__ u32x4 dequant_h(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, f16x2 zneg, f16x2 sc,
+                                           uint32_t vm) {
+  uint32_t r[4];
+  if constexpr (B == 4) {
+    const uint32_t w = cw[s];
+#pragma unroll
+    for (int i = 0; i < 4; i++) r[i] = unpack16(w, 4 * i, 0x000F000Fu, vm);
+  } else if constexpr (B == 8) {
+    const uint32_t w0 = cw[2 * s], w1 = cw[2 * s + 1];   // bytes (c0, c2, c1, c3)
+    r[0] = unpack16(w0, 0, 0x00FF00FFu, vm);
+    r[1] = unpack16(w0, 8, 0x00FF00FFu, vm);
+    r[2] = unpack16(w1, 0, 0x00FF00FFu, vm);
+    r[3] = unpack16(w1, 8, 0x00FF00FFu, vm);
+  } else if constexpr (B == 2) {
+    const uint32_t w = cw[s >> 1];
+    const int o = (s & 1) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; i++) r[i] = unpack16(w, o + 2 * i, 0x00030003u, vm);
+  } else {  // 3-bit: per 32-code block words (low plane 0-15, low plane 16-31, high plane)
+    const int blk = 3 * (s >> 2);
+    const int q = s & 3;   // octet within the block
+    const uint32_t lo = cw[blk + (q >> 1)], hi = cw[blk + 2];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int pi = 4 * q + i;   // pair index within the block
+      r[i] = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | vm;
+    }
+  }
+  u32x4 out;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const f16x2 d = __builtin_bit_cast(f16x2, r[i]) + zneg;   // q - z, exact
+    out[i] = __builtin_bit_cast(uint32_t, d * sc);            // s * (q - z), rounded once
+  }
+  return out;
+}
+
+// {s, z} word -> packed (-(1024 + z), -(1024 + z)) and (s, s).
+__device__ __forceinline__ void sz_pair(uint32_t w, f16x2& zneg, f16x2& sc) {
+  const _Float16 s16 = __builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xFFFFu));
+  const _Float16 z16 = __builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16));
+  const _Float16 zn = -(z16 + static_cast<_Float16>(1024.0f));   // exact: integer <= 1279
+  zneg = f16x2{zn, zn};
+  sc = f16x2{s16, s16};
+}
+
 template <int NM2, int NK, int BG, int BU>
-struct TCodes {
-  uint32_t cg[(kWords<NM2, BG>)];
-  uint32_t cu[(kWords<NM2, BU>)];   // unused for NK = 1
+struct HCodes {
+  uint32_t cg[(kHalfWords<NM2, BG>)];
+  uint32_t cu[(kHalfWords<NM2, BU>)];   // unused for NK = 1
   uint32_t szw[2];
 };
 
 template <int NM2, int NK, int BG, int BU>
-__device__ __forceinline__ void tile_load(TCodes<NM2, NK, BG, BU>& st, const TSrc (&src)[2], int gi, bool gv) {
+__device__ __forceinline__ void hload(HCodes<NM2, NK, BG, BU>& st, const TSrc (&src)[2], int gi, bool gv) {
   constexpr uint32_t gcb0 = NM2 * 16 * BG / 8, gcb1 = NM2 * 16 * BU / 8;   // code bytes per row and group
-  bload<kWords<NM2, BG>>(st.cg, src[0].code, gv ? src[0].coff : kOOB, gv ? gi * gcb0 : 0u);
+  bload<kHalfWords<NM2, BG>>(st.cg, src[0].code, gv ? src[0].coff : kOOB, gv ? gi * gcb0 : 0u);
   st.szw[0] = __builtin_amdgcn_raw_buffer_load_b32(src[0].sz, gv ? src[0].soff : kOOB,
                                                    gv ? gi * src[0].sz_gstride : 0u, 0);
   if constexpr (NK == 2) {
-    bload<kWords<NM2, BU>>(st.cu, src[1].code, gv ? src[1].coff : kOOB, gv ? gi * gcb1 : 0u);
+    bload<kHalfWords<NM2, BU>>(st.cu, src[1].code, gv ? src[1].coff : kOOB, gv ? gi * gcb1 : 0u);
     st.szw[1] = __builtin_amdgcn_raw_buffer_load_b32(src[1].sz, gv ? src[1].soff : kOOB,
                                                      gv ? gi * src[1].sz_gstride : 0u, 0);
   }
 }
 
-// K-step s of one kind: dequantize this lane's 8 codes and accumulate.
-template <int NM2, int B, int NW>
-__device__ __forceinline__ void tile_step(const uint32_t (&cw)[NW], int s, const u32x4& af, uint32_t vm,
-                                          uint32_t vh, f32x16& t) {
-  u32x4 wf[kPlanes<B>][NM2];
-  dequant_b<B, NM2, NW>(cw, wf, vm, vh);   // only step s survives dead-code elimination
-#pragma unroll
-  for (int pl = 0; pl < kPlanes<B>; pl++) t = mfma32(af, wf[pl][s], t);
+template <int N>
+__device__ __forceinline__ void hwait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Barrier without __syncthreads()' fences (those would drain the in-flight
+// code loads); the LDS stages are ordered by the explicit waits around it.
+__device__ __forceinline__ void tile_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 template <int NM2, int NK, int BG, int BU>
-__device__ __forceinline__ void tile_body(const FfnArgs& a, TTile<NM2>& tl, int e, int cls, int pos0, int pos1,
+__device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0, int pos1,
                                           int R, int t0, int t1) {
   constexpr int g = NM2 * 16;
-  constexpr int PPT = kTileTok * g / 8 / 256;   // 16-byte activation pieces per thread and group
-  static_assert(PPT * 256 * 8 == kTileTok * g, "tile must split evenly over the workgroup");
+  constexpr int SPT = HTile<NM2>::SPT;
+  constexpr int NLD = HTile<NM2>::SLOTS / 256;   // activation loads per thread and stage
   constexpr bool down = NK == 1;
+  // vector-memory instructions of one group's code and {s, z} loads
+  constexpr int LC = kCodeLoads<(kHalfWords<NM2, BG>)> + 1 + (NK == 2 ? kCodeLoads<(kHalfWords<NM2, BU>)> + 1 : 0);
   const int tid = threadIdx.x;
   const int wv = tid >> 6, lane = tid & 63;
-  const int wr = wv >> 1, wt = wv & 1;
   const int n = lane & 31, kh = lane >> 5;
   const bool routed = e < a.E;
   const int K = down ? (routed ? a.f : a.fs) : a.d;
@@ -814,7 +905,7 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, TTile<NM2>& tl, int 
   const int be = BG == BU ? BG : (cls == 1 ? BU : BG);
   const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
-  const int pos = pos0 + wr * 32 + n;
+  const int pos = pos0 + wv * 32 + n;
   const bool live = pos < pos1;
   const int row = live ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
 
@@ -842,113 +933,104 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, TTile<NM2>& tl, int 
     src[kk].coff = copy ? c_copy : c_base;
     src[kk].soff = copy ? s_copy : s_base;
   }
-  const float* xsum = down ? a.hsum : a.xsum;
-  const Rsrc xr = make_rsrc(down ? a.h : a.x, down ? a.h_bytes : a.x_bytes);
-  const Rsrc xsr = make_rsrc(xsum, down ? a.hsum_bytes : a.xsum_bytes);
-  // piece q = tid + 256*i of a group: token q / (g/8), column (q % (g/8)) * 8
-  const int acol = (tid % (g / 8)) * 8;
-  uint32_t arow[PPT];
+  // fp16 activations: gathered x rows (gate/up) or h rows (down), row p of the
+  // permuted order; slot i of this thread's loads
+  const Rsrc xr = make_rsrc(down ? static_cast<const void*>(a.h) : static_cast<const void*>(a.x16),
+                            down ? a.h_bytes : a.x16_bytes);
+  uint32_t aoff[NLD];
 #pragma unroll
-  for (int i = 0; i < PPT; i++) {
-    const int p = t0 + (tid + 256 * i) / (g / 8);
-    arow[i] = p < t1 ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(a.perm[p]) * K)) +
-                           2u * acol
+  for (int i = 0; i < NLD; i++) {
+    const int sl = tid + 256 * i;
+    const int t = sl / SPT;
+    const int c = (sl % SPT) ^ (t % SPT);
+    const int p = t0 + t;
+    aoff[i] = p < t1 ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(p) * K) + 16 * c)
                      : kOOB;
   }
-  const uint32_t xs_off = (tid < kTileTok && t0 + tid < t1) ? 4u * static_cast<uint32_t>(t0 + tid) : kOOB;
-  auto stage_x = [&](u32x4 (&v)[PPT], float& xsv, int gi) {
+  auto stage_a = [&](int buf, int gi) {
     const bool gv = gi < G;
-    const uint32_t xadv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
-    const uint32_t sadv = gv ? 4u * static_cast<uint32_t>(gi * a.rows) : 0u;
+    const uint32_t adv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
 #pragma unroll
-    for (int i = 0; i < PPT; i++) v[i] = bload4(xr, gv ? arow[i] : kOOB, xadv);
-    xsv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xsr, gv ? xs_off : kOOB, sadv, 0));
-  };
-  auto write_x = [&](const u32x4 (&v)[PPT], float xsv, int buf) {
-#pragma unroll
-    for (int i = 0; i < PPT; i++)
-      *reinterpret_cast<u32x4*>(&tl.x[buf][(tid + 256 * i) / (g / 8)][acol]) = v[i];
-    if (tid < kTileTok) tl.xs[buf][tid] = xsv;
+    for (int i = 0; i < NLD; i++) lds_dma16(xr, &tl.a[buf][256 * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
   };
 
-  uint32_t vm = kMagic, vh = 0x44004400u;
-  asm volatile("" : "+v"(vm), "+v"(vh));
-  f32x16 acc[NK];
+  const uint32_t vm = kMagic16;
+  f32x16 acc[NK][4];
 #pragma unroll
-  for (int kk = 0; kk < NK; kk++) acc[kk] = f32x16{};
-  // codes of the next two groups and activations of the next group in
-  // flight (deeper prefetch measured no faster here)
-  TCodes<NM2, NK, BG, BU> st[2];
-  tile_load<NM2, NK, BG, BU>(st[0], src, 0, 0 < G);
-  tile_load<NM2, NK, BG, BU>(st[1], src, 1, 1 < G);
-  u32x4 vx[PPT];
-  float vxs;
-  stage_x(vx, vxs, 0);
-  write_x(vx, vxs, 0);
-  __syncthreads();
-  const int tok_lane0 = wt * 32 + 4 * kh;   // tile token of accumulator 0 of this lane
+  for (int kk = 0; kk < NK; kk++)
+#pragma unroll
+    for (int tb = 0; tb < 4; tb++) acc[kk][tb] = f32x16{};
 
-  auto group = [&](TCodes<NM2, NK, BG, BU>& c, int buf, int gi) {
-    stage_x(vx, vxs, gi + 1);
-    if (gi < G) {   // wave-uniform
-      f32x16 t[NK];
+  HCodes<NM2, NK, BG, BU> cs[2];
+  stage_a(0, 0);
+  hload<NM2, NK, BG, BU>(cs[0], src, 0, 0 < G);
+  hload<NM2, NK, BG, BU>(cs[1], src, 1, 1 < G);
+  hwait_vm<2 * LC>();   // activations of group 0 have landed (this wave's share)
+  tile_barrier();       // ... every wave's share
+
+  auto group = [&](HCodes<NM2, NK, BG, BU>& c, int buf, int gi) {
+    stage_a(buf ^ 1, gi + 1);   // stage buf^1 was last read for group gi-1 (barrier since)
+    if (gi < G) {   // workgroup-uniform (G is odd for some shapes)
+    f16x2 zn[NK], sc[NK];
+    sz_pair(c.szw[0], zn[0], sc[0]);
+    if constexpr (NK == 2) sz_pair(c.szw[1], zn[1], sc[1]);
 #pragma unroll
-      for (int kk = 0; kk < NK; kk++) t[kk] = f32x16{};
+    for (int s = 0; s < NM2; s++) {
+      u32x4 af[4];
 #pragma unroll
-      for (int s = 0; s < NM2; s++) {
-        const u32x4 af = *reinterpret_cast<const u32x4*>(&tl.x[buf][wt * 32 + n][(g / 2) * kh + 8 * s]);
-        tile_step<NM2, BG, kWords<NM2, BG>>(c.cg, s, af, vm, vh, t[0]);
-        if constexpr (NK == 2) tile_step<NM2, BU, kWords<NM2, BU>>(c.cu, s, af, vm, vh, t[1]);
+      for (int tb = 0; tb < 4; tb++) {
+        const int t = tb * 32 + n;
+        af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
       }
-      float sc[NK], zz[NK];
-      sc[0] = fp16_bits_to_f32(c.szw[0] & 0xFFFFu);
-      zz[0] = fp16_bits_to_f32(c.szw[0] >> 16) + kOffset<BG>;
+      const u32x4 bg = dequant_h<NM2, BG>(c.cg, s, zn[0], sc[0], vm);
+#pragma unroll
+      for (int tb = 0; tb < 4; tb++) acc[0][tb] = mfma32h(af[tb], bg, acc[0][tb]);
       if constexpr (NK == 2) {
-        sc[1] = fp16_bits_to_f32(c.szw[1] & 0xFFFFu);
-        zz[1] = fp16_bits_to_f32(c.szw[1] >> 16) + kOffset<BU>;
+        const u32x4 bu = dequant_h<NM2, BU>(c.cu, s, zn[1], sc[1], vm);
+#pragma unroll
+        for (int tb = 0; tb < 4; tb++) acc[1][tb] = mfma32h(af[tb], bu, acc[1][tb]);
       }
-      f32x4 X[4];
-#pragma unroll
-      for (int q = 0; q < 4; q++) X[q] = *reinterpret_cast<const f32x4*>(&tl.xs[buf][tok_lane0 + 8 * q]);
-      __builtin_amdgcn_sched_barrier(0);
-      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int kk = 0; kk < NK; kk++)
-#pragma unroll
-        for (int r = 0; r < 16; r++)
-          acc[kk][r] = __fmaf_rn(sc[kk], __fmaf_rn(-zz[kk], X[r / 4][r % 4], t[kk][r]), acc[kk][r]);
     }
-    tile_load<NM2, NK, BG, BU>(c, src, gi + 2, gi + 2 < G);
-    write_x(vx, vxs, buf ^ 1);
-    __syncthreads();
+    }
+    hload<NM2, NK, BG, BU>(c, src, gi + 2, gi + 2 < G);
+    hwait_vm<LC>();   // everything but the code loads just issued: activations of group gi+1
+    tile_barrier();
   };
   for (int gi = 0; gi < G; gi += 2) {
-    group(st[0], 0, gi);
-    group(st[1], 1, gi + 1);
+    group(cs[0], 0, gi);
+    group(cs[1], 1, gi + 1);
   }
+  hwait_vm<0>();
 
-  // outputs: tokens t0 + tok_lane0 + 8*(r/4) + r%4, row `row`
+  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4, row `row`
   if constexpr (NK == 2) {
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-      const int p = t0 + tok_lane0 + 8 * (r / 4) + (r % 4);
-      if (live && p < t1) a.h[h_row(a, p) + row] = static_cast<uint16_t>(bf16_rne(silu_mul(acc[0][r], acc[1][r])));
-    }
+    for (int tb = 0; tb < 4; tb++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) {
+        const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
+        if (live && p < t1) {
+          // h = bf16(silu(g) * u), stored as its (exact) fp16 value
+          const float hb = __uint_as_float(bf16_rne(silu_mul(acc[0][tb][r], acc[1][tb][r])) << 16);
+          a.h[h_row(a, p) + row] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
+        }
+      }
   } else {
     for (int sp = 0; sp < a.n_split_out; sp++) {
       float* out = a.o + static_cast<int64_t>(sp) * a.split_stride;
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        const int p = t0 + tok_lane0 + 8 * (r / 4) + (r % 4);
-        if (live && p < t1) out[static_cast<int64_t>(p) * R + row] = sp == 0 ? acc[0][r] : 0.f;
-      }
+      for (int tb = 0; tb < 4; tb++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
+          if (live && p < t1) out[static_cast<int64_t>(p) * R + row] = sp == 0 ? acc[0][tb][r] : 0.f;
+        }
     }
   }
 }
 
 template <int NM2, int NK, int B>
-__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, TTile<NM2>& tl, int e, int cls, int pos0,
+__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0,
                                               int pos1, int R, int t0, int t1) {
   if constexpr (NK == 1) {
     if (cls == 0) tile_body<NM2, 1, B, B>(a, tl, e, 0, pos0, pos1, R, t0, t1);
@@ -961,10 +1043,13 @@ __device__ __forceinline__ void tile_dispatch(const FfnArgs& a, TTile<NM2>& tl, 
   }
 }
 
+// One wave per SIMD: the 128 accumulator registers of a wave's 32 rows x 128
+// tokens x 2 kinds leave no room for a second wave, and eight independent
+// accumulator chains per wave keep the matrix core busy on their own.
 template <int NM2, int NK>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
 ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
-  __shared__ __attribute__((aligned(16))) TTile<NM2> tl;
+  __shared__ __attribute__((aligned(16))) HTile<NM2> tl;
   __shared__ int pre[MOE_MAX_EXPERTS + 1];
   for (int i = threadIdx.x; i <= map.n_e; i += blockDim.x) pre[i] = prefix[i];
   __syncthreads();
@@ -1029,7 +1114,7 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
     else if (B == 2) tile_dispatch<NM2, NK, 2>(a, tl, e, cls, pos0, pos1, R, t0, t1);
     else if constexpr (NM2 % 4 == 0) tile_dispatch<NM2, NK, 3>(a, tl, e, cls, pos0, pos1, R, t0, t1);
-    __syncthreads();   // the LDS tile is reused by the next item
+    tile_barrier();   // the LDS stages are reused by the next item
   }
 }
 
@@ -1070,12 +1155,32 @@ group_sum_kernel(FfnArgs a, const uint16_t* __restrict__ in, const int32_t* __re
   if (live && q == 0) out[static_cast<int64_t>(j) * a.rows + p] = s;
 }
 
+// x16[p][c] = fp16(x[perm[p]][c]) for permuted rows p0 <= p < p1, the
+// activation operand of the tile kernel (exact for |x| < 65504, the bf16
+// values being a subset of fp16's in that range); 8 values per thread.
+__global__ void __launch_bounds__(256) gather_f16_kernel(FfnArgs a, int p0, int p1) {
+  const int per_row = a.d / 8;
+  const int64_t id = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (id >= static_cast<int64_t>(p1 - p0) * per_row) return;
+  const int p = p0 + static_cast<int>(id / per_row);
+  const int c = static_cast<int>(id % per_row) * 8;
+  const u32x4 v = *reinterpret_cast<const u32x4*>(a.x + static_cast<int64_t>(a.perm[p]) * a.d + c);
+  u32x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<_Float16>(bf16_lo(v[i])));
+    const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<_Float16>(bf16_hi(v[i])));
+    o[i] = lo | (hi << 16);
+  }
+  *reinterpret_cast<u32x4*>(const_cast<uint16_t*>(a.x16) + static_cast<int64_t>(p) * a.d + c) = o;
+}
+
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 struct Plan {
   int n_split;
   int nt_routed, nt_shared;   // token tiles of the streaming kernel, 0: tile kernel
-  size_t xsum_bytes, h_bytes, hsum_bytes, tile_bytes, total;
+  size_t xsum_bytes, h_bytes, hsum_bytes, tile_bytes, x16_bytes, total;
 };
 
 // Streaming kernel for up to 28 expected tokens per expert (one or two
@@ -1108,7 +1213,9 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   p.h_bytes = align256(sizeof(uint16_t) * static_cast<size_t>(hcols));
   p.hsum_bytes = align256(sizeof(float) * static_cast<size_t>(rows) * (fmax / g));
   p.tile_bytes = align256(sizeof(int32_t) * 4 * (MOE_MAX_EXPERTS + 1));
-  p.total = p.xsum_bytes + p.h_bytes + p.hsum_bytes + p.tile_bytes + 256;
+  const bool tiled = p.nt_routed == 0 || (S > 0 && p.nt_shared == 0);
+  p.x16_bytes = tiled ? align256(sizeof(uint16_t) * static_cast<size_t>(rows) * L->d_model) : 0;
+  p.total = p.xsum_bytes + p.h_bytes + p.hsum_bytes + p.tile_bytes + p.x16_bytes + 256;
   return p;
 }
 
@@ -1205,8 +1312,8 @@ TileMap tile_map(const moe_layer_t* L, bool shared) {
   return m;
 }
 
-// Persistent tile grid: two workgroups per compute unit, a multiple of the
-// XCD count.
+// Persistent tile grid: one workgroup per compute unit (the tile kernel runs
+// one wave per SIMD), a multiple of the XCD count.
 int tile_grid() {
   static int cached[64] = {0};
   int dev = 0;
@@ -1214,7 +1321,7 @@ int tile_grid() {
   if (cached[dev] == 0) {
     int cu = 0;
     if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
-    cached[dev] = std::max(kXcds, (2 * cu) / kXcds * kXcds);
+    cached[dev] = std::max(kXcds, cu / kXcds * kXcds);
   }
   return cached[dev];
 }
@@ -1249,13 +1356,25 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   const int S = a.S;
   auto event = [&](int i) -> hipEvent_t { return (ev && i < n_ev) ? ev[i] : nullptr; };
   std::vector<Launch> xsum, gate_up, hsum, down;
-  {  // group sums of the gathered activations, [d/g][rows]
-    const int64_t n = static_cast<int64_t>(a.rows) * (a.d / g) * (g / 8);
-    xsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-      klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
-              a, a.x, a.perm, static_cast<int64_t>(a.d), 0, a.rows, a.d, const_cast<float*>(a.xsum));
-    });
-  }
+  // activation preparation per row range: group sums [d/g][rows] for the
+  // streaming kernel, fp16 copies for the tile kernel
+  auto prep = [&](int p0, int p1, bool tiled) {
+    if (p1 <= p0) return;
+    if (tiled) {
+      const int64_t n = static_cast<int64_t>(p1 - p0) * (a.d / 8);
+      xsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(gather_f16_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1, a, p0, p1);
+      });
+    } else {
+      const int64_t n = static_cast<int64_t>(p1 - p0) * (a.d / g) * (g / 8);
+      xsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
+                a, a.x, a.perm, static_cast<int64_t>(a.d), p0, p1, a.d, const_cast<float*>(a.xsum));
+      });
+    }
+  };
+  prep(0, a.Tk, p.nt_routed == 0);
+  if (S > 0) prep(a.Tk, a.rows, p.nt_shared == 0);
   int32_t* prefix = a.tile_prefix;
   auto add = [&](std::vector<Launch>& v, auto nk, bool shared, int nt, int nsplit) {
     constexpr int NK = decltype(nk)::value;
@@ -1286,15 +1405,15 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   using one = std::integral_constant<int, 1>;
   add(gate_up, two{}, false, p.nt_routed, 1);
   if (S > 0) add(gate_up, two{}, true, p.nt_shared, 1);
-  {  // group sums of h, [max(f,fs)/g][rows]
-    const int64_t n = static_cast<int64_t>(a.Tk) * (a.f / g) * (g / 8);
+  {  // group sums of h, [max(f,fs)/g][rows], for the rows the streaming kernel reads
+    const int64_t n = p.nt_routed != 0 ? static_cast<int64_t>(a.Tk) * (a.f / g) * (g / 8) : 0;
     if (n > 0)
       hsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
         klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
                 a, static_cast<const uint16_t*>(a.h), static_cast<const int32_t*>(nullptr),
                 int64_t{0}, 0, a.Tk, a.f, a.hsum);
       });
-    if (S > 0) {
+    if (S > 0 && p.nt_shared != 0) {
       const int64_t n2 = static_cast<int64_t>(a.rows - a.Tk) * (a.fs / g) * (g / 8);
       hsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
         klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n2, 256))), dim3(256), s, e0,
@@ -1371,6 +1490,7 @@ int ffn_entry(const moe_layer_t* L, const uint16_t* x, int32_t T, int32_t k,
   a.h = reinterpret_cast<uint16_t*>(w + p.xsum_bytes);
   a.hsum = reinterpret_cast<float*>(w + p.xsum_bytes + p.h_bytes);
   a.tile_prefix = reinterpret_cast<int32_t*>(w + p.xsum_bytes + p.h_bytes + p.hsum_bytes);
+  a.x16 = reinterpret_cast<const uint16_t*>(w + p.xsum_bytes + p.h_bytes + p.hsum_bytes + p.tile_bytes);
   a.n_split_out = p.n_split;
   a.o = o;
   a.split_stride = static_cast<int64_t>(T) * (k + L->n_shared) * L->d_model;
@@ -1378,8 +1498,9 @@ int ffn_entry(const moe_layer_t* L, const uint16_t* x, int32_t T, int32_t k,
     const int64_t lim = int64_t{1} << 31;
     const int64_t xb = static_cast<int64_t>(T) * L->d_model * 2;
     if (xb >= lim || static_cast<int64_t>(p.h_bytes) >= lim || static_cast<int64_t>(p.xsum_bytes) >= lim ||
-        static_cast<int64_t>(p.hsum_bytes) >= lim)
+        static_cast<int64_t>(p.hsum_bytes) >= lim || static_cast<int64_t>(p.x16_bytes) >= lim)
       return MOE_ERR_ARG;
+    a.x16_bytes = static_cast<uint32_t>(p.x16_bytes);
     a.x_bytes = static_cast<uint32_t>(xb);
     a.h_bytes = static_cast<uint32_t>(p.h_bytes);
     a.xsum_bytes = static_cast<uint32_t>(p.xsum_bytes);

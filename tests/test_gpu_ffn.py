@@ -3,10 +3,17 @@ the channel switch -> combine) against the oracle.
 
 Tolerance: relative L2 <= 2e-3 on the layer output, per workload and per
 mask epoch (the stated bound for bf16 inputs with fp32 accumulation).  The
-oracle carries the one rounding point of the method's arithmetic (h in bf16),
-so the observed error is fp32 accumulation order plus rare one-ulp flips of
-h; a tighter diagnostic bound (5e-4) is asserted too: measured 1e-5..2e-4,
-largest for the K = 14336 down projection of the Mixtral-shaped layer.
+oracle carries the exact dequantized weights and the one rounding point of
+the method's arithmetic (h in bf16).  Two kernels compute the FFN:
+
+- the streaming kernel (experts with few tokens) contracts the exact
+  weights, so its error is fp32 accumulation order plus rare one-ulp flips
+  of h: diagnostic bound 5e-4 where every row streams (measured 1e-5..2e-4);
+- the tile kernel (experts with many tokens, e.g. shared experts or
+  prefill) rounds each dequantized weight to fp16, the paper's 16-bit
+  dequantized operand; the relative error of ~2e-4 per weight flips h's
+  bf16 rounding more often: diagnostic bound 1.5e-3 (measured 1.0e-3 ..
+  1.2e-3, the CPU study of fp16-rounded weights predicts 1.0e-3..1.1e-3).
 """
 import numpy as np
 import pytest
@@ -18,6 +25,8 @@ from gpu_util import dev, oracle_row_slots, rel_l2, routing_matches, to_dev_bf16
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-3
+DIAG_STREAM = 5e-4   # every row through the streaming kernel (exact weights)
+DIAG_TILE = 1.5e-3   # rows through the fp16 tile kernel
 
 
 def _layer(name):
@@ -114,11 +123,12 @@ def _sampled_parity(orc, name, n_tok, seed=0):
 
 
 def test_deepseek_decode_parity(orc):
-    assert _sampled_parity(orc, "deepseek-decode", 48) <= 5e-4
+    # routed experts stream; the two shared experts see all 128 tokens and tile
+    assert _sampled_parity(orc, "deepseek-decode", 48) <= DIAG_TILE
 
 
 def test_mixtral_decode_parity(orc):
-    assert _sampled_parity(orc, "mixtral-decode", 24) <= 5e-4
+    assert _sampled_parity(orc, "mixtral-decode", 24) <= DIAG_STREAM
 
 
 def test_ffn_run_to_run_deterministic():
@@ -133,13 +143,13 @@ def test_ffn_run_to_run_deterministic():
 
 def test_mixtral_prefill_parity(orc):
     # 4096 tokens, Zipf-skewed loads: experts with up to ~3300 rows, many
-    # 64-token tiles per expert
-    _sampled_parity(orc, "mixtral-prefill", 12)
+    # 128-token tiles per expert
+    assert _sampled_parity(orc, "mixtral-prefill", 12) <= DIAG_TILE
 
 
 def test_deepseek_prefill_parity(orc):
     # 8192 tokens, 64 routed experts + 2 shared experts over all tokens
-    _sampled_parity(orc, "deepseek-prefill", 12)
+    assert _sampled_parity(orc, "deepseek-prefill", 12) <= DIAG_TILE
 
 
 def test_qwen_stress_mask_redraws(orc):
@@ -167,4 +177,4 @@ def test_qwen_stress_mask_redraws(orc):
         print("qwen step", step, "epoch", epoch, "switched %d%%" % inp.switch_percent(epoch),
               "rel_l2", err, flush=True)
         assert err <= TOL
-        assert err <= 5e-4
+        assert err <= DIAG_TILE   # 512 tokens over 60 experts: the tile kernel
