@@ -698,7 +698,7 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
 // ------------------------------------------------------------------ tile kernel
 // For experts with many tokens (prefill, shared experts), where the
 // contraction is MFMA-bound: a workgroup computes a tile of kTileTok tokens x
-// kTileRows row positions (per kind) with v_mfma_f32_32x32x16_f16.  This is
+// kTileRowsOf<NK> row positions with v_mfma_f32_32x32x16_f16.  This is
 // the paper's formulation of the dequantized product (Sec. V-B: dequantize to
 // a 16-bit operand, then matrix-core multiply): the weight operand is
 // fp16(s * (q - z)) -- one rounding per weight -- and the activations enter
@@ -710,15 +710,15 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
 // exactly 1024 + q (q < 1024); one packed fp16 subtraction of 1024 + z makes
 // q - z exactly, one packed fp16 multiplication by s rounds the product.
 //
-// Wave w owns rows [32w, 32w + 32) of the tile and all kTileTok tokens (four
-// 32-token blocks): every dequantized B fragment feeds four MFMAs per kind,
-// and every A fragment (from LDS) NK.  Lane l holds row l % 32 and the K-half
-// l/32 of each group (group code g/2*half + 8*s + j feeds K-step s, slot j);
-// accumulator element r of lane l is token 8*(r/4) + 4*(l/32) + r%4 of the
-// block.  The activations of one group for the whole tile are staged in LDS
-// by direct-to-LDS loads, double-buffered, with the XOR swizzle of the
-// streaming kernel; the packed codes of the next group are in flight in
-// registers.
+// Wave w owns 32 rows (gate/up: both kinds of them) or 64 rows (down) of the
+// tile and all kTileTok tokens (four 32-token blocks): every dequantized B
+// fragment feeds four MFMAs and every A fragment (from LDS) two.  Lane l holds
+// row l % 32 of each 32-row block and the K-half l/32 of each group (group
+// code g/2*half + 8*s + j feeds K-step s, slot j); accumulator element r of
+// lane l is token 8*(r/4) + 4*(l/32) + r%4 of the block.  The activations of
+// one group for the whole tile are staged in LDS by direct-to-LDS loads, two
+// groups ahead (three stages), with the XOR swizzle of the streaming kernel;
+// the packed codes of the next three groups are in flight in registers.
 //
 // Work items (expert, row block, token tile) come from a prefix table a small
 // plan kernel builds from the routing offsets and class counts, and are
@@ -738,12 +738,22 @@ __device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const 
 }
 
 constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token blocks)
-constexpr int kTileRows = 128;  // row positions per workgroup tile and kind (4 waves x 32)
+
+// Weight fragments per K-step of one wave: NK kinds of RB 32-row blocks.
+// Gate/up: both kinds of the same 32 rows (RB = 1); down: 64 rows (RB = 2),
+// so that every A fragment read from LDS feeds eight MFMAs either way.
+template <int NK>
+constexpr int kTileRB = NK == 2 ? 1 : 2;
+
+// Row positions per workgroup tile (four waves).
+template <int NK>
+constexpr int kTileRowsOf = 4 * 32 * kTileRB<NK>;
+
 constexpr int kXcds = 8;
 constexpr int kSuper = 8;
 constexpr uint32_t kMagic16 = 0x64006400u;   // two fp16 1024.0
 
-// LDS of the tile kernel: two stages of kTileTok token rows x g columns of
+// LDS of the tile kernel: three stages of kTileTok token rows x g columns of
 // fp16 activations in 16-byte slots (slot s: token s / (g/8), column chunk
 // (s % (g/8)) ^ (token % (g/8))).
 template <int NM2>
@@ -751,7 +761,7 @@ struct HTile {
   static constexpr int g = NM2 * 16;
   static constexpr int SPT = g / 8;
   static constexpr int SLOTS = kTileTok * SPT;
-  u32x4 a[2][SLOTS];
+  u32x4 a[3][SLOTS];
 };
 
 // Experts e0 .. e0+n_e-1 of one tile launch; bits[e - e0].
@@ -774,9 +784,9 @@ __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, 
     int blocks = 0;
     if (e < a.E) {
       const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
-      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) blocks += (cc[c] + kTileRows - 1) / kTileRows;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) blocks += (cc[c] + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
     } else {
-      blocks = (NK == 1 ? a.d : a.fs) / kTileRows;
+      blocks = ((NK == 1 ? a.d : a.fs) + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
     }
     items = tiles * blocks;
   }
@@ -857,23 +867,39 @@ __device__ __forceinline__ void sz_pair(uint32_t w, f16x2& zneg, f16x2& sc) {
   sc = f16x2{s16, s16};
 }
 
-template <int NM2, int NK, int BG, int BU>
+// Code width of fragment j: kinds gate (BG) and up (BU), or the blocks of
+// one kind.
+template <int NK, int BG, int BU>
+__host__ __device__ constexpr int frag_bits(int j) {
+  return NK == 2 ? (j == 0 ? BG : BU) : BG;
+}
+
+constexpr int kMaxHalfWords = 16;   // 8-bit codes, g = 128
+
+template <int NM2, int J>
 struct HCodes {
-  uint32_t cg[(kHalfWords<NM2, BG>)];
-  uint32_t cu[(kHalfWords<NM2, BU>)];   // unused for NK = 1
-  uint32_t szw[2];
+  uint32_t cw[J][kMaxHalfWords];   // only the first kHalfWords<NM2, width> are used
+  uint32_t szw[J];
 };
 
 template <int NM2, int NK, int BG, int BU>
-__device__ __forceinline__ void hload(HCodes<NM2, NK, BG, BU>& st, const TSrc (&src)[2], int gi, bool gv) {
-  constexpr uint32_t gcb0 = NM2 * 16 * BG / 8, gcb1 = NM2 * 16 * BU / 8;   // code bytes per row and group
-  bload<kHalfWords<NM2, BG>>(st.cg, src[0].code, gv ? src[0].coff : kOOB, gv ? gi * gcb0 : 0u);
-  st.szw[0] = __builtin_amdgcn_raw_buffer_load_b32(src[0].sz, gv ? src[0].soff : kOOB,
-                                                   gv ? gi * src[0].sz_gstride : 0u, 0);
-  if constexpr (NK == 2) {
-    bload<kHalfWords<NM2, BU>>(st.cu, src[1].code, gv ? src[1].coff : kOOB, gv ? gi * gcb1 : 0u);
-    st.szw[1] = __builtin_amdgcn_raw_buffer_load_b32(src[1].sz, gv ? src[1].soff : kOOB,
-                                                     gv ? gi * src[1].sz_gstride : 0u, 0);
+__device__ __forceinline__ void hload(HCodes<NM2, NK * kTileRB<NK>>& st, const TSrc (&src)[2], int gi, bool gv) {
+  constexpr int J = NK * kTileRB<NK>;
+#pragma unroll
+  for (int j = 0; j < J; j++) {
+    const int bw = frag_bits<NK, BG, BU>(j);
+    const TSrc& sr = src[j];
+    const uint32_t gcb = static_cast<uint32_t>(NM2 * 16 * bw / 8);   // code bytes per row and group
+    uint32_t(&cw)[kMaxHalfWords] = st.cw[j];
+    if (bw == 8) bload<kHalfWords<NM2, 8>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 8>]>(&cw), sr.code,
+                                           gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
+    else if (bw == 4) bload<kHalfWords<NM2, 4>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 4>]>(&cw), sr.code,
+                                                gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
+    else if (bw == 2) bload<kHalfWords<NM2, 2>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 2>]>(&cw), sr.code,
+                                                gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
+    else if constexpr (NM2 == 8) bload<kHalfWords<NM2, 3>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 3>]>(&cw),
+                                                            sr.code, gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
+    st.szw[j] = __builtin_amdgcn_raw_buffer_load_b32(sr.sz, gv ? sr.soff : kOOB, gv ? gi * sr.sz_gstride : 0u, 0);
   }
 }
 
@@ -887,17 +913,30 @@ __device__ __forceinline__ void hwait_vm() {
 // code loads); the LDS stages are ordered by the explicit waits around it.
 __device__ __forceinline__ void tile_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// silu(g) * u with a hardware reciprocal: h is rounded to bf16 right after,
+// far coarser than the reciprocal's error.
+__device__ __forceinline__ float silu_mul_fast(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
+
+// Activation stages in flight: the stage of group gi+2 is loaded while group
+// gi is contracted; three LDS stages.
+constexpr int kAStages = 3;
+
 template <int NM2, int NK, int BG, int BU>
 __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0, int pos1,
                                           int R, int t0, int t1) {
   constexpr int g = NM2 * 16;
   constexpr int SPT = HTile<NM2>::SPT;
   constexpr int NLD = HTile<NM2>::SLOTS / 256;   // activation loads per thread and stage
+  constexpr int RB = kTileRB<NK>;
+  constexpr int J = NK * RB;
   constexpr bool down = NK == 1;
   // vector-memory instructions of one group's code and {s, z} loads
-  constexpr int LC = kCodeLoads<(kHalfWords<NM2, BG>)> + 1 + (NK == 2 ? kCodeLoads<(kHalfWords<NM2, BU>)> + 1 : 0);
+  constexpr int LC = kCodeLoads<(kHalfWords<NM2, frag_bits<NK, BG, BU>(0)>)> + 1 +
+                     (J == 2 ? kCodeLoads<(kHalfWords<NM2, frag_bits<NK, BG, BU>(1)>)> + 1 : 0);
   const int tid = threadIdx.x;
-  const int wv = tid >> 6, lane = tid & 63;
+  const int wv = uni(static_cast<int>(tid >> 6)), lane = tid & 63;   // wave index in a scalar register
   const int n = lane & 31, kh = lane >> 5;
   const bool routed = e < a.E;
   const int K = down ? (routed ? a.f : a.fs) : a.d;
@@ -905,13 +944,20 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
   const int be = BG == BU ? BG : (cls == 1 ? BU : BG);
   const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
-  const int pos = pos0 + wv * 32 + n;
-  const bool live = pos < pos1;
-  const int row = live ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+  int row[RB];
+  bool live[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; rb++) {
+    const int pos = pos0 + wv * 32 * RB + 32 * rb + n;
+    live[rb] = pos < pos1;
+    row[rb] = live[rb] ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+  }
 
   TSrc src[2];
 #pragma unroll
-  for (int kk = 0; kk < NK; kk++) {
+  for (int j = 0; j < J; j++) {
+    const int kk = NK == 2 ? j : 0;
+    const int rb = NK == 2 ? 0 : j;
     const KindDev& kd = a.kd[kind0 + kk];
     const bool copy = (cls >> kk) & 1;
     const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
@@ -922,16 +968,16 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
                             : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
     const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
     const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
-    src[kk].code = make_rsrc(cptr, cbytes);
-    src[kk].sz = make_rsrc(sptr, sbytes);
-    src[kk].sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
-    const int slot = (copy && live) ? kd.row_slot[static_cast<int64_t>(e) * R + row] : -1;
-    const uint32_t c_base = live ? row * row_bytes + kh * (g / 2) * be / 8 : kOOB;
-    const uint32_t s_base = live ? row * 4u : kOOB;
+    src[j].code = make_rsrc(cptr, cbytes);
+    src[j].sz = make_rsrc(sptr, sbytes);
+    src[j].sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
+    const int slot = (copy && live[rb]) ? kd.row_slot[static_cast<int64_t>(e) * R + row[rb]] : -1;
+    const uint32_t c_base = live[rb] ? row[rb] * row_bytes + kh * (g / 2) * be / 8 : kOOB;
+    const uint32_t s_base = live[rb] ? row[rb] * 4u : kOOB;
     const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * crow_bytes + kh * (g / 2) : kOOB;
     const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
-    src[kk].coff = copy ? c_copy : c_base;
-    src[kk].soff = copy ? s_copy : s_base;
+    src[j].coff = copy ? c_copy : c_base;
+    src[j].soff = copy ? s_copy : s_base;
   }
   // fp16 activations: gathered x rows (gate/up) or h rows (down), row p of the
   // permuted order; slot i of this thread's loads
@@ -954,77 +1000,87 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
     for (int i = 0; i < NLD; i++) lds_dma16(xr, &tl.a[buf][256 * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
   };
 
-  const uint32_t vm = kMagic16;
-  f32x16 acc[NK][4];
+  // the OR operand of the unpacking in a vector register (one v_and_or_b32)
+  uint32_t vm = kMagic16;
+  asm volatile("" : "+v"(vm));
+  f32x16 acc[J][4];
 #pragma unroll
-  for (int kk = 0; kk < NK; kk++)
+  for (int j = 0; j < J; j++)
 #pragma unroll
-    for (int tb = 0; tb < 4; tb++) acc[kk][tb] = f32x16{};
+    for (int tb = 0; tb < 4; tb++) acc[j][tb] = f32x16{};
 
-  HCodes<NM2, NK, BG, BU> cs[2];
+  HCodes<NM2, J> cs[3];
   stage_a(0, 0);
   hload<NM2, NK, BG, BU>(cs[0], src, 0, 0 < G);
+  stage_a(1, 1);
   hload<NM2, NK, BG, BU>(cs[1], src, 1, 1 < G);
-  hwait_vm<2 * LC>();   // activations of group 0 have landed (this wave's share)
-  tile_barrier();       // ... every wave's share
+  hload<NM2, NK, BG, BU>(cs[2], src, 2, 2 < G);
+  hwait_vm<2 * LC + NLD>();   // activations of group 0 have landed (this wave's share)
+  tile_barrier();             // ... every wave's share
 
-  auto group = [&](HCodes<NM2, NK, BG, BU>& c, int buf, int gi) {
-    stage_a(buf ^ 1, gi + 1);   // stage buf^1 was last read for group gi-1 (barrier since)
+  auto group = [&](HCodes<NM2, J>& c, int buf, int gi) {
+    stage_a((buf + 2) % kAStages, gi + 2);   // that stage was last read for group gi-1 (barrier since)
     if (gi < G) {   // workgroup-uniform (G is odd for some shapes)
-    f16x2 zn[NK], sc[NK];
-    sz_pair(c.szw[0], zn[0], sc[0]);
-    if constexpr (NK == 2) sz_pair(c.szw[1], zn[1], sc[1]);
+      f16x2 zn[J], sc[J];
 #pragma unroll
-    for (int s = 0; s < NM2; s++) {
-      u32x4 af[4];
+      for (int j = 0; j < J; j++) sz_pair(c.szw[j], zn[j], sc[j]);
 #pragma unroll
-      for (int tb = 0; tb < 4; tb++) {
-        const int t = tb * 32 + n;
-        af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
-      }
-      const u32x4 bg = dequant_h<NM2, BG>(c.cg, s, zn[0], sc[0], vm);
+      for (int s = 0; s < NM2; s++) {
+        u32x4 af[4];
 #pragma unroll
-      for (int tb = 0; tb < 4; tb++) acc[0][tb] = mfma32h(af[tb], bg, acc[0][tb]);
-      if constexpr (NK == 2) {
-        const u32x4 bu = dequant_h<NM2, BU>(c.cu, s, zn[1], sc[1], vm);
+        for (int tb = 0; tb < 4; tb++) {
+          const int t = tb * 32 + n;
+          af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
+        }
 #pragma unroll
-        for (int tb = 0; tb < 4; tb++) acc[1][tb] = mfma32h(af[tb], bu, acc[1][tb]);
+        for (int j = 0; j < J; j++) {
+          u32x4 bf;
+          const int bw = frag_bits<NK, BG, BU>(j);
+          if (bw == 8) bf = dequant_h<NM2, 8>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 8>]>(&c.cw[j]), s, zn[j], sc[j], vm);
+          else if (bw == 4) bf = dequant_h<NM2, 4>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 4>]>(&c.cw[j]), s, zn[j], sc[j], vm);
+          else if (bw == 2) bf = dequant_h<NM2, 2>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 2>]>(&c.cw[j]), s, zn[j], sc[j], vm);
+          else if constexpr (NM2 == 8) bf = dequant_h<NM2, 3>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 3>]>(&c.cw[j]), s, zn[j], sc[j], vm);
+#pragma unroll
+          for (int tb = 0; tb < 4; tb++) acc[j][tb] = mfma32h(af[tb], bf, acc[j][tb]);
+        }
       }
     }
-    }
-    hload<NM2, NK, BG, BU>(c, src, gi + 2, gi + 2 < G);
-    hwait_vm<LC>();   // everything but the code loads just issued: activations of group gi+1
+    hload<NM2, NK, BG, BU>(c, src, gi + 3, gi + 3 < G);
+    hwait_vm<2 * LC + NLD>();   // everything but the last two code loads and the newest stage: group gi+1's
     tile_barrier();
   };
-  for (int gi = 0; gi < G; gi += 2) {
+  for (int gi = 0; gi < G; gi += 3) {
     group(cs[0], 0, gi);
     group(cs[1], 1, gi + 1);
+    group(cs[2], 2, gi + 2);
   }
   hwait_vm<0>();
 
-  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4, row `row`
+  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4
   if constexpr (NK == 2) {
 #pragma unroll
     for (int tb = 0; tb < 4; tb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
-        if (live && p < t1) {
+        if (live[0] && p < t1) {
           // h = bf16(silu(g) * u), stored as its (exact) fp16 value
-          const float hb = __uint_as_float(bf16_rne(silu_mul(acc[0][tb][r], acc[1][tb][r])) << 16);
-          a.h[h_row(a, p) + row] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
+          const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc[0][tb][r], acc[1][tb][r])) << 16);
+          a.h[h_row(a, p) + row[0]] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
         }
       }
   } else {
     for (int sp = 0; sp < a.n_split_out; sp++) {
       float* out = a.o + static_cast<int64_t>(sp) * a.split_stride;
 #pragma unroll
-      for (int tb = 0; tb < 4; tb++)
+      for (int rb = 0; rb < RB; rb++)
 #pragma unroll
-        for (int r = 0; r < 16; r++) {
-          const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
-          if (live && p < t1) out[static_cast<int64_t>(p) * R + row] = sp == 0 ? acc[0][tb][r] : 0.f;
-        }
+        for (int tb = 0; tb < 4; tb++)
+#pragma unroll
+          for (int r = 0; r < 16; r++) {
+            const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
+            if (live[rb] && p < t1) out[static_cast<int64_t>(p) * R + row[rb]] = sp == 0 ? acc[rb][tb][r] : 0.f;
+          }
     }
   }
 }
@@ -1076,9 +1132,9 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     int n_rb = 0;
     if (routed) {
       const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
-      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) n_rb += (uni(cc[c]) + kTileRows - 1) / kTileRows;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) n_rb += (uni(cc[c]) + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
     } else {
-      n_rb = R / kTileRows;
+      n_rb = (R + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
     }
     const int full = (n_rb / kSuper) * kSuper * tiles;
     int rb, tt;
@@ -1096,7 +1152,7 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
       const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
       for (int c = 0; c < (NK == 1 ? 2 : 4); c++) {
         const int cn = uni(cc[c]);
-        const int nb = (cn + kTileRows - 1) / kTileRows;
+        const int nb = (cn + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
         if (rb < nb) {
           cls = c;
           count = cn;
@@ -1106,8 +1162,8 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
         start += cn;
       }
     }
-    const int pos0 = start + rb * kTileRows;
-    const int pos1 = min(pos0 + kTileRows, start + count);
+    const int pos0 = start + rb * kTileRowsOf<NK>;
+    const int pos1 = min(pos0 + kTileRowsOf<NK>, start + count);
     const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
     const int B = map.bits[e - map.e0];
     if (B == 8) tile_dispatch<NM2, NK, 8>(a, tl, e, cls, pos0, pos1, R, t0, t1);
