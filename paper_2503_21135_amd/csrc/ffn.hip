@@ -710,15 +710,17 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
 // exactly 1024 + q (q < 1024); one packed fp16 subtraction of 1024 + z makes
 // q - z exactly, one packed fp16 multiplication by s rounds the product.
 //
-// Wave w owns 32 rows (gate/up: both kinds of them) or 64 rows (down) of the
-// tile and all kTileTok tokens (four 32-token blocks): every dequantized B
-// fragment feeds four MFMAs and every A fragment (from LDS) two.  Lane l holds
-// row l % 32 of each 32-row block and the K-half l/32 of each group (group
-// code g/2*half + 8*s + j feeds K-step s, slot j); accumulator element r of
-// lane l is token 8*(r/4) + 4*(l/32) + r%4 of the block.  The activations of
-// one group for the whole tile are staged in LDS by direct-to-LDS loads, two
-// groups ahead (three stages), with the XOR swizzle of the streaming kernel;
-// the packed codes of the next three groups are in flight in registers.
+// Eight waves per workgroup, two per SIMD.  Each wave owns 32 rows of one
+// kind (gate/up: waves 0-3 the gate rows, 4-7 the up rows of the tile's 128
+// positions; down: 256 rows) and all kTileTok tokens (four 32-token blocks),
+// so every dequantized B fragment feeds four MFMAs.  Lane l holds row l % 32
+// and the K-half l/32 of each group (group code g/2*half + 8*s + j feeds
+// K-step s, slot j); accumulator element r of lane l is token
+// 8*(r/4) + 4*(l/32) + r%4 of the block.  The activations of one group for
+// the whole tile are staged in LDS by direct-to-LDS loads, two groups ahead
+// (three stages), with the XOR swizzle of the streaming kernel; the packed
+// codes of the next three groups are in flight in registers.  The SiLU-GLU
+// epilogue meets the gate and up sums of a row through LDS.
 //
 // Work items (expert, row block, token tile) come from a prefix table a small
 // plan kernel builds from the routing offsets and class counts, and are
@@ -739,15 +741,12 @@ __device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const 
 
 constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token blocks)
 
-// Weight fragments per K-step of one wave: NK kinds of RB 32-row blocks.
-// Gate/up: both kinds of the same 32 rows (RB = 1); down: 64 rows (RB = 2),
-// so that every A fragment read from LDS feeds eight MFMAs either way.
+// Row positions per workgroup tile: eight waves of 32 rows, gate/up split
+// over the waves by kind (128 rows of both kinds) or down (256 rows).
 template <int NK>
-constexpr int kTileRB = NK == 2 ? 1 : 2;
+constexpr int kTileRowsOf = NK == 2 ? 128 : 256;
 
-// Row positions per workgroup tile (four waves).
-template <int NK>
-constexpr int kTileRowsOf = 4 * 32 * kTileRB<NK>;
+constexpr int kTileWaves = 8;
 
 constexpr int kXcds = 8;
 constexpr int kSuper = 8;
@@ -761,7 +760,10 @@ struct HTile {
   static constexpr int g = NM2 * 16;
   static constexpr int SPT = g / 8;
   static constexpr int SLOTS = kTileTok * SPT;
-  u32x4 a[3][SLOTS];
+  union {
+    u32x4 a[3][SLOTS];
+    float xch[4 * 4 * 16 * 64];   // gate/up epilogue: the up sums of four 32-row blocks
+  };
 };
 
 // Experts e0 .. e0+n_e-1 of one tile launch; bits[e - e0].
@@ -867,40 +869,17 @@ __device__ __forceinline__ void sz_pair(uint32_t w, f16x2& zneg, f16x2& sc) {
   sc = f16x2{s16, s16};
 }
 
-// Code width of fragment j: kinds gate (BG) and up (BU), or the blocks of
-// one kind.
-template <int NK, int BG, int BU>
-__host__ __device__ constexpr int frag_bits(int j) {
-  return NK == 2 ? (j == 0 ? BG : BU) : BG;
-}
-
-constexpr int kMaxHalfWords = 16;   // 8-bit codes, g = 128
-
-template <int NM2, int J>
+template <int NM2, int BW>
 struct HCodes {
-  uint32_t cw[J][kMaxHalfWords];   // only the first kHalfWords<NM2, width> are used
-  uint32_t szw[J];
+  uint32_t cw[(kHalfWords<NM2, BW>)];
+  uint32_t szw;
 };
 
-template <int NM2, int NK, int BG, int BU>
-__device__ __forceinline__ void hload(HCodes<NM2, NK * kTileRB<NK>>& st, const TSrc (&src)[2], int gi, bool gv) {
-  constexpr int J = NK * kTileRB<NK>;
-#pragma unroll
-  for (int j = 0; j < J; j++) {
-    const int bw = frag_bits<NK, BG, BU>(j);
-    const TSrc& sr = src[j];
-    const uint32_t gcb = static_cast<uint32_t>(NM2 * 16 * bw / 8);   // code bytes per row and group
-    uint32_t(&cw)[kMaxHalfWords] = st.cw[j];
-    if (bw == 8) bload<kHalfWords<NM2, 8>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 8>]>(&cw), sr.code,
-                                           gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
-    else if (bw == 4) bload<kHalfWords<NM2, 4>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 4>]>(&cw), sr.code,
-                                                gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
-    else if (bw == 2) bload<kHalfWords<NM2, 2>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 2>]>(&cw), sr.code,
-                                                gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
-    else if constexpr (NM2 == 8) bload<kHalfWords<NM2, 3>>(*reinterpret_cast<uint32_t(*)[kHalfWords<NM2, 3>]>(&cw),
-                                                            sr.code, gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
-    st.szw[j] = __builtin_amdgcn_raw_buffer_load_b32(sr.sz, gv ? sr.soff : kOOB, gv ? gi * sr.sz_gstride : 0u, 0);
-  }
+template <int NM2, int BW>
+__device__ __forceinline__ void hload(HCodes<NM2, BW>& st, const TSrc& sr, int gi, bool gv) {
+  constexpr uint32_t gcb = NM2 * 16 * BW / 8;   // code bytes per row and group
+  bload<kHalfWords<NM2, BW>>(st.cw, sr.code, gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
+  st.szw = __builtin_amdgcn_raw_buffer_load_b32(sr.sz, gv ? sr.soff : kOOB, gv ? gi * sr.sz_gstride : 0u, 0);
 }
 
 template <int N>
@@ -923,43 +902,33 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 // gi is contracted; three LDS stages.
 constexpr int kAStages = 3;
 
-template <int NM2, int NK, int BG, int BU>
-__device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0, int pos1,
-                                          int R, int t0, int t1) {
+// One wave's share of a tile item: 32 rows (position block rb) of weight kind
+// kk, whose source has width BW (the expert's base width, or 8 for the
+// cached copies of a switched class), against all kTileTok tokens.
+template <int NM2, int NK, int BW>
+__device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int e, bool copy, int be, int kk,
+                                          int rb, int pos0, int pos1, int R, int t0, int t1) {
   constexpr int g = NM2 * 16;
   constexpr int SPT = HTile<NM2>::SPT;
-  constexpr int NLD = HTile<NM2>::SLOTS / 256;   // activation loads per thread and stage
-  constexpr int RB = kTileRB<NK>;
-  constexpr int J = NK * RB;
+  constexpr int NLD = HTile<NM2>::SLOTS / (64 * kTileWaves);   // activation loads per thread and stage
   constexpr bool down = NK == 1;
   // vector-memory instructions of one group's code and {s, z} loads
-  constexpr int LC = kCodeLoads<(kHalfWords<NM2, frag_bits<NK, BG, BU>(0)>)> + 1 +
-                     (J == 2 ? kCodeLoads<(kHalfWords<NM2, frag_bits<NK, BG, BU>(1)>)> + 1 : 0);
+  constexpr int LC = kCodeLoads<(kHalfWords<NM2, BW>)> + 1;
   const int tid = threadIdx.x;
-  const int wv = uni(static_cast<int>(tid >> 6)), lane = tid & 63;   // wave index in a scalar register
+  const int wv = tid >> 6, lane = tid & 63;
   const int n = lane & 31, kh = lane >> 5;
   const bool routed = e < a.E;
   const int K = down ? (routed ? a.f : a.fs) : a.d;
   const int G = K / g;
-  const int be = BG == BU ? BG : (cls == 1 ? BU : BG);
   const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
-  int row[RB];
-  bool live[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; rb++) {
-    const int pos = pos0 + wv * 32 * RB + 32 * rb + n;
-    live[rb] = pos < pos1;
-    row[rb] = live[rb] ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
-  }
+  const int pos = pos0 + 32 * rb + n;
+  const bool live = pos < pos1;
+  const int row = live ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
 
-  TSrc src[2];
-#pragma unroll
-  for (int j = 0; j < J; j++) {
-    const int kk = NK == 2 ? j : 0;
-    const int rb = NK == 2 ? 0 : j;
+  TSrc src;
+  {
     const KindDev& kd = a.kd[kind0 + kk];
-    const bool copy = (cls >> kk) & 1;
     const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
     const uint32_t crow_bytes = 4u * static_cast<uint32_t>(code_row_words(K, 8));
     const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
@@ -968,16 +937,16 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
                             : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
     const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
     const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
-    src[j].code = make_rsrc(cptr, cbytes);
-    src[j].sz = make_rsrc(sptr, sbytes);
-    src[j].sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
-    const int slot = (copy && live[rb]) ? kd.row_slot[static_cast<int64_t>(e) * R + row[rb]] : -1;
-    const uint32_t c_base = live[rb] ? row[rb] * row_bytes + kh * (g / 2) * be / 8 : kOOB;
-    const uint32_t s_base = live[rb] ? row[rb] * 4u : kOOB;
+    src.code = make_rsrc(cptr, cbytes);
+    src.sz = make_rsrc(sptr, sbytes);
+    src.sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
+    const int slot = (copy && live) ? kd.row_slot[static_cast<int64_t>(e) * R + row] : -1;
+    const uint32_t c_base = live ? row * row_bytes + kh * (g / 2) * be / 8 : kOOB;
+    const uint32_t s_base = live ? row * 4u : kOOB;
     const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * crow_bytes + kh * (g / 2) : kOOB;
     const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
-    src[j].coff = copy ? c_copy : c_base;
-    src[j].soff = copy ? s_copy : s_base;
+    src.coff = copy ? c_copy : c_base;
+    src.soff = copy ? s_copy : s_base;
   }
   // fp16 activations: gathered x rows (gate/up) or h rows (down), row p of the
   // permuted order; slot i of this thread's loads
@@ -986,7 +955,7 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
   uint32_t aoff[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; i++) {
-    const int sl = tid + 256 * i;
+    const int sl = tid + 64 * kTileWaves * i;
     const int t = sl / SPT;
     const int c = (sl % SPT) ^ (t % SPT);
     const int p = t0 + t;
@@ -997,33 +966,31 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
     const bool gv = gi < G;
     const uint32_t adv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
 #pragma unroll
-    for (int i = 0; i < NLD; i++) lds_dma16(xr, &tl.a[buf][256 * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
+    for (int i = 0; i < NLD; i++)
+      lds_dma16(xr, &tl.a[buf][64 * kTileWaves * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
   };
 
   // the OR operand of the unpacking in a vector register (one v_and_or_b32)
   uint32_t vm = kMagic16;
   asm volatile("" : "+v"(vm));
-  f32x16 acc[J][4];
+  f32x16 acc[4];
 #pragma unroll
-  for (int j = 0; j < J; j++)
-#pragma unroll
-    for (int tb = 0; tb < 4; tb++) acc[j][tb] = f32x16{};
+  for (int tb = 0; tb < 4; tb++) acc[tb] = f32x16{};
 
-  HCodes<NM2, J> cs[3];
+  HCodes<NM2, BW> cs[3];
   stage_a(0, 0);
-  hload<NM2, NK, BG, BU>(cs[0], src, 0, 0 < G);
+  hload<NM2, BW>(cs[0], src, 0, 0 < G);
   stage_a(1, 1);
-  hload<NM2, NK, BG, BU>(cs[1], src, 1, 1 < G);
-  hload<NM2, NK, BG, BU>(cs[2], src, 2, 2 < G);
+  hload<NM2, BW>(cs[1], src, 1, 1 < G);
+  hload<NM2, BW>(cs[2], src, 2, 2 < G);
   hwait_vm<2 * LC + NLD>();   // activations of group 0 have landed (this wave's share)
   tile_barrier();             // ... every wave's share
 
-  auto group = [&](HCodes<NM2, J>& c, int buf, int gi) {
+  auto group = [&](HCodes<NM2, BW>& c, int buf, int gi) {
     stage_a((buf + 2) % kAStages, gi + 2);   // that stage was last read for group gi-1 (barrier since)
     if (gi < G) {   // workgroup-uniform (G is odd for some shapes)
-      f16x2 zn[J], sc[J];
-#pragma unroll
-      for (int j = 0; j < J; j++) sz_pair(c.szw[j], zn[j], sc[j]);
+      f16x2 zn, sc;
+      sz_pair(c.szw, zn, sc);
 #pragma unroll
       for (int s = 0; s < NM2; s++) {
         u32x4 af[4];
@@ -1032,20 +999,12 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
           const int t = tb * 32 + n;
           af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
         }
+        const u32x4 bf = dequant_h<NM2, BW>(c.cw, s, zn, sc, vm);
 #pragma unroll
-        for (int j = 0; j < J; j++) {
-          u32x4 bf;
-          const int bw = frag_bits<NK, BG, BU>(j);
-          if (bw == 8) bf = dequant_h<NM2, 8>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 8>]>(&c.cw[j]), s, zn[j], sc[j], vm);
-          else if (bw == 4) bf = dequant_h<NM2, 4>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 4>]>(&c.cw[j]), s, zn[j], sc[j], vm);
-          else if (bw == 2) bf = dequant_h<NM2, 2>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 2>]>(&c.cw[j]), s, zn[j], sc[j], vm);
-          else if constexpr (NM2 == 8) bf = dequant_h<NM2, 3>(*reinterpret_cast<const uint32_t(*)[kHalfWords<NM2, 3>]>(&c.cw[j]), s, zn[j], sc[j], vm);
-#pragma unroll
-          for (int tb = 0; tb < 4; tb++) acc[j][tb] = mfma32h(af[tb], bf, acc[j][tb]);
-        }
+        for (int tb = 0; tb < 4; tb++) acc[tb] = mfma32h(af[tb], bf, acc[tb]);
       }
     }
-    hload<NM2, NK, BG, BU>(c, src, gi + 3, gi + 3 < G);
+    hload<NM2, BW>(c, src, gi + 3, gi + 3 < G);
     hwait_vm<2 * LC + NLD>();   // everything but the last two code loads and the newest stage: group gi+1's
     tile_barrier();
   };
@@ -1056,54 +1015,79 @@ __device__ __forceinline__ void tile_body(const FfnArgs& a, HTile<NM2>& tl, int 
   }
   hwait_vm<0>();
 
-  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4
+  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4, row `row`
   if constexpr (NK == 2) {
+    // the up waves hand their sums to the gate waves of the same rows through
+    // the (now idle) activation stages; same lane layout on both sides
+    float* xch = tl.xch;
+    tile_barrier();   // every wave is done reading the activation stages
+    if (kk == 1) {
+#pragma unroll
+      for (int tb = 0; tb < 4; tb++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) xch[((rb * 4 + tb) * 16 + r) * 64 + lane] = acc[tb][r];
+    }
+    tile_barrier();
+    if (kk == 0) {
+      // rows of one item are all routed or all shared: one h row width
+      const int hw = t0 < a.Tk ? a.f : a.fs;
+      uint16_t* hbase = a.h + h_row(a, t0 + 4 * kh) + row;
+#pragma unroll
+      for (int tb = 0; tb < 4; tb++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+          const float u = xch[((rb * 4 + tb) * 16 + r) * 64 + lane];
+          if (live && t0 + 4 * kh + dt < t1) {
+            // h = bf16(silu(g) * u), stored as its (exact) fp16 value
+            const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc[tb][r], u)) << 16);
+            hbase[dt * hw] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
+          }
+        }
+    }
+  } else {
+    float* obase = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row;
 #pragma unroll
     for (int tb = 0; tb < 4; tb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) {
-        const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
-        if (live[0] && p < t1) {
-          // h = bf16(silu(g) * u), stored as its (exact) fp16 value
-          const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc[0][tb][r], acc[1][tb][r])) << 16);
-          a.h[h_row(a, p) + row[0]] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
-        }
+        const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+        if (live && t0 + 4 * kh + dt < t1) obase[dt * R] = acc[tb][r];
       }
-  } else {
-    for (int sp = 0; sp < a.n_split_out; sp++) {
-      float* out = a.o + static_cast<int64_t>(sp) * a.split_stride;
+    // the other split slices of these rows (the combine adds every slice)
+    for (int sp = 1; sp < a.n_split_out; sp++) {
+      float* ob = obase + static_cast<int64_t>(sp) * a.split_stride;
 #pragma unroll
-      for (int rb = 0; rb < RB; rb++)
+      for (int tb = 0; tb < 4; tb++)
 #pragma unroll
-        for (int tb = 0; tb < 4; tb++)
-#pragma unroll
-          for (int r = 0; r < 16; r++) {
-            const int p = t0 + tb * 32 + 8 * (r / 4) + 4 * kh + (r % 4);
-            if (live[rb] && p < t1) out[static_cast<int64_t>(p) * R + row[rb]] = sp == 0 ? acc[rb][tb][r] : 0.f;
-          }
+        for (int r = 0; r < 16; r++) {
+          const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+          if (live && t0 + 4 * kh + dt < t1) ob[dt * R] = 0.f;
+        }
     }
   }
 }
 
+// Waves 0-3 take the gate rows and waves 4-7 the up rows of the tile's 128
+// positions, or all eight waves take 32 of the 256 down rows; a kind whose
+// class bit is set reads the 8-bit copies.
 template <int NM2, int NK, int B>
 __device__ __forceinline__ void tile_dispatch(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0,
                                               int pos1, int R, int t0, int t1) {
-  if constexpr (NK == 1) {
-    if (cls == 0) tile_body<NM2, 1, B, B>(a, tl, e, 0, pos0, pos1, R, t0, t1);
-    else tile_body<NM2, 1, 8, 8>(a, tl, e, 1, pos0, pos1, R, t0, t1);
-  } else {
-    if (cls == 0) tile_body<NM2, 2, B, B>(a, tl, e, 0, pos0, pos1, R, t0, t1);
-    else if (cls == 1) tile_body<NM2, 2, 8, B>(a, tl, e, 1, pos0, pos1, R, t0, t1);
-    else if (cls == 2) tile_body<NM2, 2, B, 8>(a, tl, e, 2, pos0, pos1, R, t0, t1);
-    else tile_body<NM2, 2, 8, 8>(a, tl, e, 3, pos0, pos1, R, t0, t1);
-  }
+  const int wv = threadIdx.x >> 6;
+  const int kk = NK == 2 ? wv / 4 : 0;
+  const int rb = NK == 2 ? wv % 4 : wv;
+  const bool copy = (cls >> kk) & 1;
+  // the expert's base width: class 1 or 2 has one kind on copies, whose
+  // template width is 8 even though the base width is B
+  if (copy) tile_wave<NM2, NK, 8>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+  else tile_wave<NM2, NK, B>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
 }
 
-// One wave per SIMD: the 128 accumulator registers of a wave's 32 rows x 128
-// tokens x 2 kinds leave no room for a second wave, and eight independent
-// accumulator chains per wave keep the matrix core busy on their own.
+// Eight waves, two per SIMD: a wave's 64 accumulator registers leave room for
+// a second wave, which hides the first one's load and LDS latencies.
 template <int NM2, int NK>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
 ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
   __shared__ __attribute__((aligned(16))) HTile<NM2> tl;
   __shared__ int pre[MOE_MAX_EXPERTS + 1];
@@ -1443,7 +1427,7 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
         klaunch(tile_plan_kernel<NK>, dim3(1), dim3(256), s, e0, e1, a, m, const_cast<int32_t*>(pf));
       });
       v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-        klaunch(ffn_tile_kernel<2 * NM, NK>, dim3(static_cast<unsigned>(tile_grid())), dim3(256), s,
+        klaunch(ffn_tile_kernel<2 * NM, NK>, dim3(static_cast<unsigned>(tile_grid())), dim3(64 * kTileWaves), s,
                 e0, e1, a, m, pf);
       });
       return;
