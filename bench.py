@@ -182,6 +182,146 @@ def cpu_baseline(wk, inputs, batch, min_seconds):
                          inputs.switch_percent(0), reps * len(rows), tok, k, dt)}
 
 
+PREFILL_OF = {"mixtral-decode": "mixtral-prefill", "deepseek-decode": "deepseek-prefill"}
+
+
+def measure_prefill(layer, inputs, name, hip, steps, warmup):
+    """The same packed layer at prefill: whole-step time and the gate/up
+    launch (the MFMA-bound kernel) against the bf16/fp16 matrix-core peak."""
+    import torch
+    import moe_inputs as mi
+    from paper_2503_21135_amd import api
+    wk = mi.WORKLOADS[name]
+    batch = mi.make_batch(wk, inputs)
+    x = torch.from_numpy(batch.x.view(np.int16)).to("cuda:0").view(torch.bfloat16)
+    bias = None if batch.bias is None else torch.from_numpy(batch.bias).to("cuda:0")
+    b = layer.buffers(wk.tokens)
+    for _ in range(warmup):
+        layer.route(x, bias)
+        layer.ffn(x, b)
+        layer.combine(b)
+    torch.cuda.synchronize()
+    ev = hip.create(2 * steps)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        layer.route(x, bias)
+        api.moe_expert_ffn_mixed_ev(layer.desc, x, layer.k, b.offsets, b.perm, b.o, b.ffn_ws,
+                                    (C.c_void_p * 5)(None, ev[2 * i], ev[2 * i + 1], None, None))
+        layer.combine(b)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    gu = float(np.mean([hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(steps)]))
+    hip.destroy(ev)
+    off = b.offsets.cpu().numpy()
+    fgu = flops_gate_up(layer, off)
+    tf = fgu / (gu * 1e-3) / 1e12
+    return {"workload": "%s: T=%d, router biased to Zipf s=%s loads" % (name, wk.tokens, wk.zipf_s)
+            if wk.zipf_s else "%s: T=%d" % (name, wk.tokens),
+            "tokens_per_s": round(wk.tokens / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
+            "steps": steps,
+            "roofline": {"bound": "mfma", "kernel": "FFN gate/up stage (tile kernel, fp16 operands)",
+                         "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / BF16_PEAK_TFLOPS, 4), "avg_launch_ms": round(gu, 4),
+                         "algorithmic_flops_per_launch": int(fgu)},
+            "layer_tflops": round(algorithmic_flops(layer, off) / (ms * 1e-3) / 1e12, 1),
+            "expert_rows": [int(v) for v in np.diff(off)]}
+
+
+def measure_graph(layer, x, bias, b, y_eager, steps):
+    """One decode step captured in a HIP graph and replayed; every replay's
+    output is checked against the eager step's (bitwise: the path is
+    deterministic)."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        layer.route(x, bias)
+        layer.ffn(x, b)
+        layer.combine(b)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        layer.route(x, bias)
+        layer.ffn(x, b)
+        layer.combine(b)
+    ok = True
+    for _ in range(3):   # replays with eager work and synchronisation between them
+        b.y.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        ok = ok and bool(torch.equal(b.y, y_eager))
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        g.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    ok = ok and bool(torch.equal(b.y, y_eager))
+    ms = t0.elapsed_time(t1) / steps
+    return {"ms_per_step": round(ms, 5), "tokens_per_s": round(x.shape[0] / (ms * 1e-3), 1),
+            "replays_match_eager": ok}
+
+
+def measure_switch(layer, inputs, wk, hip, steps):
+    """The mask-redraw workload: a fresh batch every step, the switch mask
+    redrawn every `redraw_every` steps.  Steady tokens/s excludes the
+    switch; switch latency is the host wall time of installing one epoch's
+    slot lists (three moe_set_channel_switch calls) until the stream is idle,
+    and its device time from events."""
+    import torch
+    import moe_inputs as mi
+    from paper_2503_21135_amd import api
+    n_ep = (steps + wk.redraw_every - 1) // wk.redraw_every
+    slots = [[np.ascontiguousarray(inputs.slots_on(kd, ep), np.int32) for kd in range(3)]
+             for ep in range(n_ep)]
+    xs = []
+    for st in range(min(steps, 20)):   # distinct batches, reused cyclically
+        bt = mi.make_batch(wk, inputs, step=st)
+        xs.append(torch.from_numpy(bt.x.view(np.int16)).to("cuda:0").view(torch.bfloat16))
+    b = layer.buffers(wk.tokens)
+    sptr = torch.cuda.current_stream().cuda_stream
+    ev = hip.create(2 * steps + 2 * n_ep)
+    host_sw = []
+    ep_i = 0
+    torch.cuda.synchronize()
+    for st in range(steps):
+        if st % wk.redraw_every == 0:
+            ep = st // wk.redraw_every
+            torch.cuda.synchronize()
+            w0 = time.perf_counter()
+            hip.record(ev[2 * steps + 2 * ep_i], sptr)
+            for kd in range(3):
+                api.moe_set_channel_switch(layer.desc, kd, slots[ep][kd])
+            hip.record(ev[2 * steps + 2 * ep_i + 1], sptr)
+            torch.cuda.synchronize()
+            host_sw.append(time.perf_counter() - w0)
+            ep_i += 1
+        x = xs[st % len(xs)]
+        hip.record(ev[2 * st], sptr)
+        layer.route(x)
+        layer.ffn(x, b)
+        layer.combine(b)
+        hip.record(ev[2 * st + 1], sptr)
+    torch.cuda.synchronize()
+    step_ms = np.array([hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(steps)])
+    sw_dev = np.array([hip.ms(ev[2 * steps + 2 * i], ev[2 * steps + 2 * i + 1]) for i in range(ep_i)])
+    hip.destroy(ev)
+    med = float(np.median(step_ms))
+    return {"workload": "%s: T=%d x %d steps, mask redrawn every %d steps (%d epochs)"
+            % (wk.name, wk.tokens, steps, wk.redraw_every, n_ep),
+            "steady_tokens_per_s": round(wk.tokens / (med * 1e-3), 1),
+            "step_ms_median": round(med, 4), "step_ms_p10": round(float(np.percentile(step_ms, 10)), 4),
+            "step_ms_p90": round(float(np.percentile(step_ms, 90)), 4),
+            "switch_host_ms_median": round(float(np.median(host_sw)) * 1e3, 4),
+            "switch_device_ms_median": round(float(np.median(sw_dev)), 4),
+            "switched_percent_by_epoch": [int(inputs.switch_percent(e)) for e in range(n_ep)]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -191,6 +331,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="minimum CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the companion prefill measurement of a decode workload")
+    ap.add_argument("--prefill-steps", type=int, default=20)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device-to-device copies of MIB MiB (the "
                          "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -304,6 +447,24 @@ def main():
     log("gate/up %.1f GB/s %.1f TFLOP/s; FFN %.1f GB/s; %.2f TFLOP/s" %
         (achieved_gbs, achieved_tf, ffn_gbs, flops / (ffn_ms * 1e-3) / 1e12))
 
+    extra = {}
+    if wk.tokens <= 1024 and not wk.redraw_every:
+        layer.route(x, bias)
+        layer.ffn(x, b)
+        layer.combine(b)
+        torch.cuda.synchronize()
+        y_eager = b.y.clone()
+        extra["hip_graph"] = measure_graph(layer, x, bias, b, y_eager, K)
+        log("hip graph", extra["hip_graph"])
+    if wk.redraw_every:
+        extra["mask_redraw"] = measure_switch(layer, inputs, wk, hip, wk.steps)
+        log("mask redraw", extra["mask_redraw"])
+    if not args.no_prefill and args.workload in PREFILL_OF:
+        log("prefill on the same packed layer: %s" % PREFILL_OF[args.workload])
+        extra["prefill"] = measure_prefill(layer, inputs, PREFILL_OF[args.workload], hip,
+                                           args.prefill_steps, 5)
+        log("prefill", extra["prefill"])
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle for at least %.0f s ..." % args.cpu_seconds)
@@ -340,6 +501,7 @@ def main():
         "config": describe(wk),
         "roofline": roof,
         "cpu_baseline": cpu,
+        **extra,
         "detail": {
             "host_enqueue_ms_per_step": round(enqueue / K * 1e3, 5),
             "diagnostic_step_ms": round(float(layer_ms.mean()), 5),

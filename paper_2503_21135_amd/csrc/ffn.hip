@@ -689,6 +689,18 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
   if (blk * rows >= count) return;
   const int pos1 = min(pos0 + rows, start + count);
   const int B = map.bits[e - map.e0];
+  if constexpr (NT == 2) {
+    // an expert with at most 16 tokens needs one 16-token tile: half the
+    // contraction and epilogue work of the 32-token tile (same LDS)
+    if (uni(o1) - uni(o0) <= 16) {
+      auto& t1 = *reinterpret_cast<XTile<NM, 1>*>(&tl);
+      if (B == 8) dispatch_class<NM, 1, NK, 8>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      else if (B == 4) dispatch_class<NM, 1, NK, 4>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      else if (B == 2) dispatch_class<NM, 1, NK, 2>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      else if constexpr (NM == 4) dispatch_class<NM, 1, NK, 3>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      return;
+    }
+  }
   if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
