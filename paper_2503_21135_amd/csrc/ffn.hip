@@ -917,12 +917,15 @@ constexpr int kAStages = 3;
 // One wave's share of a tile item: 32 rows (position block rb) of weight kind
 // kk, whose source has width BW (the expert's base width, or 8 for the
 // cached copies of a switched class), against all kTileTok tokens.
-template <int NM2, int NK, int BW>
+template <int NM2, int NK, int BW, int TB>
 __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int e, bool copy, int be, int kk,
                                           int rb, int pos0, int pos1, int R, int t0, int t1) {
   constexpr int g = NM2 * 16;
   constexpr int SPT = HTile<NM2>::SPT;
-  constexpr int NLD = HTile<NM2>::SLOTS / (64 * kTileWaves);   // activation loads per thread and stage
+  // activation slots of the tile's TB token blocks, and loads per thread and
+  // stage (slots past them are written with zeros)
+  constexpr int SL = TB * 32 * SPT;
+  constexpr int NLD = (SL + 64 * kTileWaves - 1) / (64 * kTileWaves);
   constexpr bool down = NK == 1;
   // vector-memory instructions of one group's code and {s, z} loads
   constexpr int LC = kCodeLoads<(kHalfWords<NM2, BW>)> + 1;
@@ -971,8 +974,9 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
     const int t = sl / SPT;
     const int c = (sl % SPT) ^ (t % SPT);
     const int p = t0 + t;
-    aoff[i] = p < t1 ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(p) * K) + 16 * c)
-                     : kOOB;
+    aoff[i] = (sl < SL && p < t1)
+                  ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(p) * K) + 16 * c)
+                  : kOOB;
   }
   auto stage_a = [&](int buf, int gi) {
     const bool gv = gi < G;
@@ -985,9 +989,9 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
   // the OR operand of the unpacking in a vector register (one v_and_or_b32)
   uint32_t vm = kMagic16;
   asm volatile("" : "+v"(vm));
-  f32x16 acc[4];
+  f32x16 acc[TB];
 #pragma unroll
-  for (int tb = 0; tb < 4; tb++) acc[tb] = f32x16{};
+  for (int tb = 0; tb < TB; tb++) acc[tb] = f32x16{};
 
   HCodes<NM2, BW> cs[3];
   stage_a(0, 0);
@@ -1005,15 +1009,15 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
       sz_pair(c.szw, zn, sc);
 #pragma unroll
       for (int s = 0; s < NM2; s++) {
-        u32x4 af[4];
+        u32x4 af[TB];
 #pragma unroll
-        for (int tb = 0; tb < 4; tb++) {
+        for (int tb = 0; tb < TB; tb++) {
           const int t = tb * 32 + n;
           af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
         }
         const u32x4 bf = dequant_h<NM2, BW>(c.cw, s, zn, sc, vm);
 #pragma unroll
-        for (int tb = 0; tb < 4; tb++) acc[tb] = mfma32h(af[tb], bf, acc[tb]);
+        for (int tb = 0; tb < TB; tb++) acc[tb] = mfma32h(af[tb], bf, acc[tb]);
       }
     }
     hload<NM2, BW>(c, src, gi + 3, gi + 3 < G);
@@ -1035,7 +1039,7 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
     tile_barrier();   // every wave is done reading the activation stages
     if (kk == 1) {
 #pragma unroll
-      for (int tb = 0; tb < 4; tb++)
+      for (int tb = 0; tb < TB; tb++)
 #pragma unroll
         for (int r = 0; r < 16; r++) xch[((rb * 4 + tb) * 16 + r) * 64 + lane] = acc[tb][r];
     }
@@ -1045,7 +1049,7 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
       const int hw = t0 < a.Tk ? a.f : a.fs;
       uint16_t* hbase = a.h + h_row(a, t0 + 4 * kh) + row;
 #pragma unroll
-      for (int tb = 0; tb < 4; tb++)
+      for (int tb = 0; tb < TB; tb++)
 #pragma unroll
         for (int r = 0; r < 16; r++) {
           const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
@@ -1060,7 +1064,7 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
   } else {
     float* obase = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row;
 #pragma unroll
-    for (int tb = 0; tb < 4; tb++)
+    for (int tb = 0; tb < TB; tb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
@@ -1070,7 +1074,7 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
     for (int sp = 1; sp < a.n_split_out; sp++) {
       float* ob = obase + static_cast<int64_t>(sp) * a.split_stride;
 #pragma unroll
-      for (int tb = 0; tb < 4; tb++)
+      for (int tb = 0; tb < TB; tb++)
 #pragma unroll
         for (int r = 0; r < 16; r++) {
           const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
@@ -1091,9 +1095,20 @@ __device__ __forceinline__ void tile_dispatch(const FfnArgs& a, HTile<NM2>& tl, 
   const int rb = NK == 2 ? wv % 4 : wv;
   const bool copy = (cls >> kk) & 1;
   // the expert's base width: class 1 or 2 has one kind on copies, whose
-  // template width is 8 even though the base width is B
-  if (copy) tile_wave<NM2, NK, 8>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
-  else tile_wave<NM2, NK, B>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  // template width is 8 even though the base width is B.  The token tile of
+  // the item (an expert's last tile is partial) picks one, two or four
+  // 32-token blocks.
+  const int nt = t1 - t0;
+  if (nt <= 32) {
+    if (copy) tile_wave<NM2, NK, 8, 1>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+    else tile_wave<NM2, NK, B, 1>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  } else if (nt <= 64) {
+    if (copy) tile_wave<NM2, NK, 8, 2>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+    else tile_wave<NM2, NK, B, 2>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  } else {
+    if (copy) tile_wave<NM2, NK, 8, 4>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+    else tile_wave<NM2, NK, B, 4>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  }
 }
 
 // Eight waves, two per SIMD: a wave's 64 accumulator registers leave room for
