@@ -185,7 +185,7 @@ def cpu_baseline(wk, inputs, batch, min_seconds):
 PREFILL_OF = {"mixtral-decode": "mixtral-prefill", "deepseek-decode": "deepseek-prefill"}
 
 
-def measure_prefill(layer, inputs, name, hip, steps, warmup):
+def measure_prefill(layer, inputs, name, hip, steps, warmup, bf16=True):
     """The same packed layer at prefill: whole-step time and the gate/up
     launch (the MFMA-bound kernel) against the bf16/fp16 matrix-core peak."""
     import torch
@@ -218,7 +218,12 @@ def measure_prefill(layer, inputs, name, hip, steps, warmup):
     off = b.offsets.cpu().numpy()
     fgu = flops_gate_up(layer, off)
     tf = fgu / (gu * 1e-3) / 1e12
-    return {"workload": "%s: T=%d, router biased to Zipf s=%s loads" % (name, wk.tokens, wk.zipf_s)
+    ref = None
+    if bf16:
+        ref = measure_bf16(layer, x, b, min(steps, 10))
+        ref["speedup_of_quantized"] = round(ref["ms_per_step"] / ms, 3)
+    return {"bf16_reference": ref,
+            "workload": "%s: T=%d, router biased to Zipf s=%s loads" % (name, wk.tokens, wk.zipf_s)
             if wk.zipf_s else "%s: T=%d" % (name, wk.tokens),
             "tokens_per_s": round(wk.tokens / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
             "steps": steps,
@@ -322,6 +327,67 @@ def measure_switch(layer, inputs, wk, hip, steps):
             "switched_percent_by_epoch": [int(inputs.switch_percent(e)) for e in range(n_ep)]}
 
 
+def measure_bf16(layer, x, b, steps, warmup=3):
+    """Reference point for the paper's speedup claim (its only performance
+    figure is quantized-vs-16-bit): the same expert FFNs with unquantized
+    bf16 weights of the same shapes (seeded, random: only the time is used),
+    on the same routing, through torch's library GEMMs (hipBLASLt) --
+    gather of the routed rows, gate/up/down products, SiLU-GLU, weighted
+    combine.  Not part of the product path."""
+    import torch
+    cfg = layer.cfg
+    dev = x.device
+    gen = torch.Generator(device=dev).manual_seed(1234)
+    E, S, k = layer.E, layer.S, layer.k
+    ws = []
+    for e in range(E + S):
+        f = cfg.d_ff if e < E else cfg.d_ff_shared
+        # weights stored [in][out] contiguous: the products take no transposed views
+        wg = (torch.randn(cfg.d_model, f, generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+        wu = (torch.randn(cfg.d_model, f, generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+        wd = (torch.randn(f, cfg.d_model, generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+        ws.append((wg, wu, wd))
+    off = b.offsets.cpu().tolist()
+    perm = b.perm.long()
+    out = torch.empty(perm.numel(), cfg.d_model, dtype=torch.bfloat16, device=dev)
+    w_rows = torch.ones(perm.numel(), 1, dtype=torch.float32, device=dev)
+    inv = b.inv.long()
+
+    def step():
+        xp = x.index_select(0, perm)
+        for e in range(E + S):
+            p0, p1 = off[e], off[e + 1]
+            if p1 <= p0:
+                continue
+            wg, wu, wd = ws[e]
+            xe = xp[p0:p1]
+            h = torch.nn.functional.silu(xe @ wg) * (xe @ wu)
+            out[p0:p1] = h @ wd
+        # y[t] = sum_j w[t, j] o[inv[t, j]] (+ shared rows)
+        o = out.float()
+        y = (o[inv[:, :k]] * b.topk_w.unsqueeze(-1)).sum(1)
+        if S:
+            y = y + o[inv[:, k:]].sum(1)
+        return y
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        step()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    wbytes = sum(int(w.numel()) * 2 for t in ws for w in t)
+    del ws
+    torch.cuda.empty_cache()
+    return {"ms_per_step": round(ms, 4), "tokens_per_s": round(x.shape[0] / (ms * 1e-3), 1),
+            "weight_bytes": wbytes, "kind": "bf16 weights, torch/hipBLASLt GEMMs per expert (reference)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -334,6 +400,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the companion prefill measurement of a decode workload")
     ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--no-bf16", action="store_true",
+                    help="skip the unquantized bf16 reference of the same step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device-to-device copies of MIB MiB (the "
                          "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -459,10 +527,15 @@ def main():
     if wk.redraw_every:
         extra["mask_redraw"] = measure_switch(layer, inputs, wk, hip, wk.steps)
         log("mask redraw", extra["mask_redraw"])
+    if not args.no_bf16:
+        ref = measure_bf16(layer, x, b, min(K, 50))
+        ref["speedup_of_quantized"] = round(ref["ms_per_step"] / ms_per_step, 3)
+        extra["bf16_reference"] = ref
+        log("bf16 reference", ref)
     if not args.no_prefill and args.workload in PREFILL_OF:
         log("prefill on the same packed layer: %s" % PREFILL_OF[args.workload])
         extra["prefill"] = measure_prefill(layer, inputs, PREFILL_OF[args.workload], hip,
-                                           args.prefill_steps, 5)
+                                           args.prefill_steps, 5, bf16=not args.no_bf16)
         log("prefill", extra["prefill"])
 
     cpu = None
