@@ -327,6 +327,68 @@ def measure_switch(layer, inputs, wk, hip, steps):
             "switched_percent_by_epoch": [int(inputs.switch_percent(e)) for e in range(n_ep)]}
 
 
+def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
+    """Dynamic quantization switch for a new dataset (Sec. IV-B): the cached
+    16-bit channels of all three kinds requantized at every expert's new
+    precision (moe_requant_channels), then the copy mask installed
+    (moe_set_channel_switch).  Device time from events around the six calls,
+    host time until the stream is idle.  The share compares the device time
+    with itself plus 1024 decode steps of this layer, the online measure of
+    the paper's overhead discussion (generation of 1024 tokens)."""
+    import torch
+    from paper_2503_21135_amd import api
+    cfg = layer.cfg
+    for kd in range(3):
+        layer.channel_cache(kd)   # built before any switch (Sec. V-A)
+    slots = [np.ascontiguousarray(inputs.slots_on(kd, 0), np.int32) for kd in range(3)]
+    sptr = torch.cuda.current_stream().cuda_stream
+    ev = hip.create(3 * reps)
+    host = []
+
+    def switch(eb, evs=None):
+        if evs:
+            hip.record(evs[0], sptr)
+        for kd in range(3):
+            layer.requant(kd, eb)
+        if evs:
+            hip.record(evs[1], sptr)
+        for kd in range(3):
+            api.moe_set_channel_switch(layer.desc, kd, slots[kd])
+        if evs:
+            hip.record(evs[2], sptr)
+
+    switch(inputs.dataset_bits(reps))   # warm-up
+    torch.cuda.synchronize()
+    for r in range(reps):
+        eb = inputs.dataset_bits(r)
+        w0 = time.perf_counter()
+        switch(eb, ev[3 * r:3 * r + 3])
+        torch.cuda.synchronize()
+        host.append(time.perf_counter() - w0)
+    rq = np.array([hip.ms(ev[3 * r], ev[3 * r + 1]) for r in range(reps)])
+    inst = np.array([hip.ms(ev[3 * r + 1], ev[3 * r + 2]) for r in range(reps)])
+    hip.destroy(ev)
+    if int(layer.status.item()) != 0:
+        raise RuntimeError("requantization reported status %d" % int(layer.status.item()))
+    n_slots = [int(layer.kinds[kd]["n_slots"]) for kd in range(3)]
+    Ks = [cfg.cols(kd, 0) for kd in range(3)]
+    rd = sum(n * K * 2 for n, K in zip(n_slots, Ks))
+    wr = sum(n * (K + K // cfg.group * 4) for n, K in zip(n_slots, Ks))
+    tot = float(np.median(rq + inst))
+    return {"workload": "%s: all cached channels of the three kinds requantized at a new "
+                        "dataset's per-expert bit-widths, then the copy mask installed"
+                        % cfg.name,
+            "cached_channels": n_slots,
+            "cache_mib": round(rd / 2 ** 20, 2),
+            "requant_device_ms": round(float(np.median(rq)), 4),
+            "install_device_ms": round(float(np.median(inst)), 4),
+            "total_device_ms": round(tot, 4),
+            "host_ms": round(float(np.median(host)) * 1e3, 4),
+            "requant_bytes": int(rd + wr),
+            "requant_gbs": round((rd + wr) / (float(np.median(rq)) * 1e-3) / 1e9, 1),
+            "share_vs_1024_decode_steps": round(tot / (tot + 1024 * ms_step), 6)}
+
+
 def measure_bf16(layer, x, b, steps, warmup=3):
     """Reference point for the paper's speedup claim (its only performance
     figure is quantized-vs-16-bit): the same expert FFNs with unquantized
@@ -400,6 +462,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the companion prefill measurement of a decode workload")
     ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--no-dataset-switch", action="store_true",
+                    help="skip the timing of a requantization for a new dataset")
     ap.add_argument("--no-bf16", action="store_true",
                     help="skip the unquantized bf16 reference of the same step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -537,6 +601,10 @@ def main():
         extra["prefill"] = measure_prefill(layer, inputs, PREFILL_OF[args.workload], hip,
                                            args.prefill_steps, 5, bf16=not args.no_bf16)
         log("prefill", extra["prefill"])
+    if not wk.redraw_every and not args.no_dataset_switch:
+        # last: it rewrites the layer's copies
+        extra["dataset_switch"] = measure_dataset_switch(layer, inputs, hip, ms_per_step)
+        log("dataset switch", extra["dataset_switch"])
 
     cpu = None
     if not args.no_cpu_baseline:

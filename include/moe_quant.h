@@ -12,6 +12,9 @@
  *     cached higher-precision copies located through (expert, channel) index
  *     headers (Sec. IV-B "Channel Weights Replacement based on Caching";
  *     Sec. V-A "Data Format in the Channel Cache"),
+ *   - requantization of the cached original channels at each expert's new
+ *     precision when the dataset changes (Sec. IV-B "Channel Weights
+ *     Requantization for New Datasets"),
  *   - dequantization fused with the matrix-core contraction (Sec. V-B
  *     "Channel-Grained Dequantization"), applied to the routed expert FFN.
  *
@@ -124,8 +127,9 @@ int64_t moe_code_row_words(int32_t K, int32_t bits);
  * Its scales and zeros are group-major: the {s16, z} word of (row r, group j)
  * is sz[sz_off[e] + j*R_e + r].
  *
- * Resident 8-bit copies (the channel cache of Sec. IV-B / V-A, kept here as
- * 8-bit codes quantized from the original fp32 rows): slot s holds one row of
+ * Resident copies (the channel cache of Sec. IV-B / V-A, kept in the 8-bit
+ * code format: 8-bit codes quantized from the original rows, or b-bit codes
+ * one per byte after moe_requant_channels): slot s holds one row of
  * a routed expert, K/4 words at copy_codes[s*moe_code_row_words(K, 8)], its
  * {s16, z} words at
  * copy_sz[s*(K/group) + j], and its header (expert, row) at copy_hdr[2s],
@@ -306,7 +310,7 @@ int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
                             void* const* events, int32_t n_events);
 
 /*
- * moe_set_channel_switch -- install a set of cached 8-bit copies.
+ * moe_set_channel_switch -- install a set of cached copies.
  * Sec. IV-B "Channel Weights Replacement based on Caching" and Sec. V-A "Data
  * Format in the Channel Cache": the copy of each listed slot replaces the row
  * named by its (expert, row) header; every other row of that kind reverts to
@@ -320,6 +324,40 @@ int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
  */
 int moe_set_channel_switch(moe_layer_t* L, int32_t kind,
                            const int32_t* slots_on, int32_t n_on, void* stream);
+
+/*
+ * moe_requant_channels -- requantize cached 16-bit channels into the copy
+ * slots of one kind, each at the new precision of the expert its header names.
+ * Sec. IV-B "Channel Weights Requantization for New Datasets": once the
+ * experts' precisions are determined again for a new dataset, the retained
+ * original channels of every expert whose precision changed are quantized
+ * afresh at that precision, which may be higher or lower than before; Sec.
+ * V-A: the cache of original channels lives in device memory, entries keyed by
+ * (expert, channel) headers.
+ *
+ *   kind         MOE_KIND_GATE, MOE_KIND_UP or MOE_KIND_DOWN.
+ *   cache        device binary16 [n_slots][ld_cache] (4-byte aligned,
+ *                ld_cache even and >= K): row s is the original channel named
+ *                by slot s's header (copy_hdr[2s], copy_hdr[2s+1]).
+ *   expert_bits  host int32 [n_experts]: new precision of each routed expert
+ *                in {2, 3, 4, 8}, or 0 to leave its slots untouched; read
+ *                before the call returns.
+ *   status       device int32 or NULL: set to MOE_ERR_RANGE when a scale
+ *                overflows binary16 (the group is still written).
+ * Every slot whose expert has expert_bits[e] = b > 0 is rewritten with the
+ * moe_quant_pack quantizer at b bits applied to the binary16 values of its
+ * cache row (group size L->group, exactly as moe_quant_pack with bits = b
+ * produces for those values); the b-bit codes are stored in the 8-bit copy
+ * format (one code per byte, kind[kind].copy_codes row stride
+ * moe_code_row_words(K, 8)) with their {s16, z} words in kind[kind].copy_sz,
+ * so the FFN reads them unchanged.  copy_codes and copy_sz must be writable.
+ * The switch state is not touched: rows whose slots are switched on read the
+ * new codes from the next FFN call on the same stream.  Returns MOE_ERR_SLOT
+ * for a header naming an expert outside [0, n_experts).
+ */
+int moe_requant_channels(moe_layer_t* L, int32_t kind, const uint16_t* cache,
+                         int64_t ld_cache, const int32_t* expert_bits,
+                         int32_t* status, void* stream);
 
 /*
  * moe_unpermute_combine -- y[t] = sum_j topk_w[t][j] * o[inv_perm[t][j]]

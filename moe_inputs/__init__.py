@@ -20,6 +20,7 @@ Stream numbers:
     3000 + epoch           switched fraction of a mask epoch (pool mode)
     4000 + 1000*epoch + 3*e + kind   rows of (e, kind) switched in that epoch
     5000 + step            activations of step `step` (stress workload)
+    6000 + dataset         permutation assigning bit-widths for a new dataset
 """
 from __future__ import annotations
 
@@ -150,13 +151,7 @@ class LayerInputs:
         if cfg.bits_literal is not None:
             routed = np.asarray(cfg.bits_literal, dtype=np.int32)
         else:
-            cnt = bit_counts(cfg.bit_shares, E)
-            seq: List[int] = []
-            for b in sorted(cnt, reverse=True):
-                seq += [b] * cnt[b]
-            perm = rng(seed, cfg.cfg_id, 1).permutation(E)
-            routed = np.empty(E, dtype=np.int32)
-            routed[perm] = np.asarray(seq, dtype=np.int32)
+            routed = self._assign_bits(1)
         self.bits = np.concatenate([routed, np.full(S, 8, np.int32)])
         self.router = (rng(seed, cfg.cfg_id, 0)
                        .standard_normal((E, cfg.d_model), dtype=np.float32)
@@ -164,6 +159,31 @@ class LayerInputs:
         self._pool: Dict[int, np.ndarray] = {}
         for kind in KINDS:
             self._pool[kind] = self._make_pool(kind)
+        self._cache16: Dict[int, np.ndarray] = {}
+
+    def _assign_bits(self, stream: int) -> np.ndarray:
+        cfg = self.cfg
+        E = cfg.n_experts
+        cnt = bit_counts(cfg.bit_shares, E)
+        seq: List[int] = []
+        for b in sorted(cnt, reverse=True):
+            seq += [b] * cnt[b]
+        perm = rng(self.seed, cfg.cfg_id, stream).permutation(E)
+        out = np.empty(E, dtype=np.int32)
+        out[perm] = np.asarray(seq, dtype=np.int32)
+        return out
+
+    def dataset_bits(self, dataset: int) -> np.ndarray:
+        """Per-routed-expert bit-widths for a new dataset: the same shares of
+        bit-widths as the layer's own assignment, handed to a fresh seeded
+        permutation of the experts (a stand-in for the clustering of the new
+        dataset's expert significance).  Layers with a literal assignment
+        rotate it by dataset + 1 positions."""
+        cfg = self.cfg
+        if cfg.bits_literal is not None:
+            lit = np.asarray(cfg.bits_literal, dtype=np.int32)
+            return np.roll(lit, dataset + 1)
+        return self._assign_bits(6000 + dataset)
 
     # ---- weights -------------------------------------------------------
     def weight(self, expert: int, kind: int) -> np.ndarray:
@@ -212,6 +232,22 @@ class LayerInputs:
 
     def copy_headers(self, kind: int) -> np.ndarray:
         return self._pool[kind]
+
+    def channel_cache(self, kind: int) -> np.ndarray:
+        """The retained original 16-bit channels of the copy pool of one kind,
+        in slot order: binary16 bit patterns uint16 [n_slots][K].  The fp32
+        weights stand in for a checkpoint; their binary16 values (round to
+        nearest even) stand in for its 16-bit channels."""
+        if kind in self._cache16:
+            return self._cache16[kind]
+        hdr = self._pool[kind]
+        K = self.cfg.cols(kind, 0)
+        out = np.empty((len(hdr), K), np.float16)
+        for e in np.unique(hdr[:, 0]):
+            sl = np.nonzero(hdr[:, 0] == e)[0]
+            out[sl] = self.weight(int(e), kind)[hdr[sl, 1]].astype(np.float16)
+        self._cache16[kind] = out.view(np.uint16)
+        return self._cache16[kind]
 
     def slots_on(self, kind: int, epoch: int = 0) -> np.ndarray:
         """Slots of the copy pool switched on in a mask epoch."""

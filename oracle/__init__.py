@@ -9,7 +9,9 @@ and this module only marshals numpy arrays into it.
 The arithmetic lives in ``oracle.c``; ``layer_forward`` below strings its
 steps together in the paper's order: route (Sec. II-A), quantize each expert at
 its precision (Sec. IV-A), replace switched rows by their cached copies
-(Sec. IV-B, Sec. V-A), expert FFN, combine.
+(Sec. IV-B, Sec. V-A) -- either the 8-bit copies made from the original rows
+or the cached 16-bit channels requantized at their expert's precision for a
+new dataset (``requant_channels``, Sec. IV-B) -- expert FFN, combine.
 """
 from __future__ import annotations
 
@@ -212,6 +214,42 @@ def switch_state(layer, epoch: int = 0, kinds=(0, 1, 2)) -> Dict[int, np.ndarray
     return out
 
 
+def fp16_values(h: np.ndarray) -> np.ndarray:
+    """binary16 bit patterns -> float32 values (exact)."""
+    return np.ascontiguousarray(h, np.uint16).view(np.float16).astype(np.float32)
+
+
+def requant_channels(cache16: np.ndarray, hdr: np.ndarray, expert_bits: np.ndarray,
+                     group: int):
+    """Requantization of cached 16-bit channels for a new dataset (Sec. IV-B):
+    every cached channel whose expert has a new precision b = expert_bits[e] > 0
+    is quantized afresh at b bits from its binary16 values, with the same
+    group-wise quantizer as the experts themselves (Sec. IV-A).
+
+    cache16  uint16 binary16 patterns [n][K], row s = channel of header hdr[s]
+    Returns (status, touched bool [n], q uint8 [n][K], s16, z16 uint16 [n][K/g]);
+    rows not touched hold zeros.
+    """
+    cache16 = np.ascontiguousarray(cache16, np.uint16)
+    hdr = np.ascontiguousarray(hdr, np.int32).reshape(-1, 2)
+    n, K = cache16.shape
+    G = K // group
+    eb = np.asarray(expert_bits, np.int32)
+    bits_of = eb[hdr[:, 0]]
+    q = np.zeros((n, K), np.uint8)
+    s16 = np.zeros((n, G), np.uint16)
+    z16 = np.zeros((n, G), np.uint16)
+    status = OK
+    for b in np.unique(bits_of):
+        if b == 0:
+            continue
+        sl = np.nonzero(bits_of == b)[0]
+        st, qb, sb, zb = quantize(fp16_values(cache16[sl]), int(b), group)
+        status = min(status, st)
+        q[sl], s16[sl], z16[sl] = qb, sb, zb
+    return status, bits_of > 0, q, s16, z16
+
+
 # ---------------------------------------------------------------------------
 # FFN and combine
 # ---------------------------------------------------------------------------
@@ -243,18 +281,25 @@ def combine(o: np.ndarray, inv: np.ndarray, w: np.ndarray, k: int, S: int) -> np
 
 
 def effective_weight(w_fp32: np.ndarray, bits: int, group: int,
-                     switched_rows: Optional[np.ndarray] = None) -> np.ndarray:
+                     switched_rows: Optional[np.ndarray] = None,
+                     copy_bits: int = 0, copy_src16: Optional[np.ndarray] = None) -> np.ndarray:
     """Dequantized expert matrix as the FFN sees it: base codes at `bits`,
-    except the switched rows, which read their 8-bit copy quantized from the
-    original fp32 row (Sec. IV-B: the cache keeps the original channels; the
-    copy here is their 8-bit quantization)."""
+    except the switched rows, which read their cached copy (Sec. IV-B: the
+    cache keeps the original channels).  With copy_bits == 0 the copy is the
+    8-bit quantization of the original fp32 row; with copy_bits = b > 0 it is
+    the b-bit requantization of the cached binary16 channel copy_src16[i] of
+    switched row i (requantization for a new dataset, Sec. IV-B)."""
     st, q, s, z = quantize(w_fp32, bits, group)
     if st != OK:
         raise ValueError("oracle quantize: status %d" % st)
     W = dequant(q, s, z, group)
     if switched_rows is not None and len(switched_rows):
         rows = np.asarray(switched_rows, np.int64)
-        st, q8, s8, z8 = quantize(w_fp32[rows], 8, group)
+        if copy_bits:
+            src, b = fp16_values(copy_src16), copy_bits
+        else:
+            src, b = w_fp32[rows], 8
+        st, q8, s8, z8 = quantize(src, b, group)
         if st != OK:
             raise ValueError("oracle quantize: status %d" % st)
         W[rows] = dequant(q8, s8, z8, group)
@@ -264,11 +309,15 @@ def effective_weight(w_fp32: np.ndarray, bits: int, group: int,
 def layer_forward(layer, x_bits: np.ndarray, bias: Optional[np.ndarray] = None,
                   row_slot: Optional[Dict[int, np.ndarray]] = None,
                   round_h: bool = True, tokens: Optional[np.ndarray] = None,
-                  weight_cache: Optional[dict] = None):
+                  weight_cache: Optional[dict] = None,
+                  copy_bits: Optional[Dict[int, np.ndarray]] = None):
     """One MoE layer on the CPU.
 
     layer     moe_inputs.LayerInputs (weights are drawn from it)
     row_slot  {kind: int32 [E][R]} switch state (-1 = base), or None
+    copy_bits {kind: int32 [E]} precision of each expert's cached copies: 0 =
+              8-bit copies of the fp32 rows, b > 0 = b-bit requantization of
+              the cached 16-bit channels (layer.channel_cache), or None
     tokens    optional subset of token indices whose outputs are computed
               (routing is always done for all tokens)
     Returns dict with logits, topk_ids, topk_w, offsets, perm, inv and y
@@ -294,10 +343,15 @@ def layer_forward(layer, x_bits: np.ndarray, bias: Optional[np.ndarray] = None,
             if weight_cache is not None and key in weight_cache:
                 Ws.append(weight_cache[key])
                 continue
-            sw = None
+            sw, cb, src = None, 0, None
             if row_slot is not None and e < E:
                 sw = np.nonzero(row_slot[kind][e] >= 0)[0]
-            W = effective_weight(layer.weight(e, kind), int(layer.bits[e]), cfg.group, sw)
+                if copy_bits is not None and kind in copy_bits:
+                    cb = int(copy_bits[kind][e])
+                if cb and len(sw):
+                    src = layer.channel_cache(kind)[row_slot[kind][e][sw]]
+            W = effective_weight(layer.weight(e, kind), int(layer.bits[e]), cfg.group, sw,
+                                 cb, src)
             if weight_cache is not None:
                 weight_cache[key] = W
             Ws.append(W)

@@ -21,7 +21,7 @@ EXPORTS = (
     "moe_quant_pack", "moe_code_row_words", "moe_route_permute", "moe_route_workspace_bytes",
     "moe_ffn_plan",
     "moe_expert_ffn_mixed", "moe_expert_ffn_mixed_ev", "moe_set_channel_switch",
-    "moe_unpermute_combine", "moe_status_str",
+    "moe_requant_channels", "moe_unpermute_combine", "moe_status_str",
 )
 
 
@@ -74,6 +74,7 @@ def load() -> C.CDLL:
         "moe_expert_ffn_mixed_ev": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
                                               sz_t, vp, vp, i32]),
         "moe_set_channel_switch": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i32, vp]),
+        "moe_requant_channels": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i64, vp, vp, vp]),
         "moe_unpermute_combine": (C.c_int, [vp, i32, i64, vp, vp, i32, i32, i32, i32, vp, vp]),
         "moe_status_str": (C.c_char_p, [C.c_int]),
     }

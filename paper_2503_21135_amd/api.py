@@ -110,7 +110,7 @@ def moe_expert_ffn_mixed_ev(desc: LayerDesc, x: torch.Tensor, k: int, offsets: t
 
 def moe_set_channel_switch(desc: LayerDesc, kind: int, slots_on: Optional[np.ndarray],
                            stream=None) -> None:
-    """Install cached 8-bit copies by (expert, row) header (Sec. IV-B, V-A)."""
+    """Install cached copies by (expert, row) header (Sec. IV-B, V-A)."""
     if slots_on is None or len(slots_on) == 0:
         arr, ptr, n = None, None, 0
     else:
@@ -118,6 +118,26 @@ def moe_set_channel_switch(desc: LayerDesc, kind: int, slots_on: Optional[np.nda
         ptr, n = arr.ctypes.data_as(C.c_void_p), int(arr.size)
     st = load().moe_set_channel_switch(C.byref(desc), kind, ptr, n, _s(stream))
     check(st, "moe_set_channel_switch")
+
+
+def moe_requant_channels(desc: LayerDesc, kind: int, cache: torch.Tensor,
+                         expert_bits: np.ndarray, status: Optional[torch.Tensor] = None,
+                         stream=None) -> None:
+    """Requantize the cached 16-bit channels of one kind into its copy slots at
+    each expert's new precision (Sec. IV-B, requantization for new datasets).
+
+    cache        device float16 [n_slots][K] (row s = original channel of slot s)
+    expert_bits  int [n_experts], 0 = leave that expert's slots as they are
+    """
+    _need_cuda(cache, status)
+    if cache.dtype != torch.float16 or cache.dim() != 2 or cache.stride(1) != 1:
+        raise MoEError("cache must be a row-major float16 matrix")
+    eb = np.ascontiguousarray(expert_bits, dtype=np.int32)
+    if eb.size != desc.n_experts:
+        raise MoEError("expert_bits needs one entry per routed expert")
+    st = load().moe_requant_channels(C.byref(desc), kind, _p(cache), cache.stride(0),
+                                     eb.ctypes.data_as(C.c_void_p), _p(status), _s(stream))
+    check(st, "moe_requant_channels")
 
 
 def moe_unpermute_combine(o: torch.Tensor, n_split: int, inv_perm: torch.Tensor,

@@ -1,8 +1,11 @@
 // pack.hip -- moe_quant_pack: group-wise asymmetric uniform quantization of
-// fp32 rows and packing of the codes into 32-bit words.
+// fp32 rows and packing of the codes into 32-bit words; moe_requant_channels:
+// the same quantizer applied to cached 16-bit channels, written into the
+// 8-bit copy slots the FFN reads.
 //
-// Sec. IV-A (each expert quantized uniformly at its precision) and Sec. V-B
-// (several low-bit codes loaded as one 32-bit word).  The quantizer and the
+// Sec. IV-A (each expert quantized uniformly at its precision), Sec. V-B
+// (several low-bit codes loaded as one 32-bit word) and Sec. IV-B
+// (requantization of the cached channels for a new dataset).  The quantizer and the
 // word layout are defined in moe_quant.h; parameter math is binary64, which
 // gfx950 rounds exactly as IEEE requires, so the codes are reproducible bit
 // for bit on any IEEE host.
@@ -106,6 +109,88 @@ pack_kernel(const float* __restrict__ w, int64_t ld_w, int K, int bits, int grou
   }
 }
 
+
+// Per-expert target precision of a requantization, passed by value
+// (0 = the expert's slots are left as they are).
+struct ExpertBits {
+  uint8_t b[MOE_MAX_EXPERTS];
+};
+
+// One wave per (copy slot, group).  Lane l holds group/64 consecutive fp16
+// values of the cached row; the range, scale, zero and codes follow the same
+// binary64 quantizer as pack_kernel, so a row requantized at b bits carries
+// exactly the codes moe_quant_pack gives for its binary16 values.  The b-bit
+// codes are stored in the 8-bit copy format: each byte holds one code, bytes
+// of a word in the 8-bit half-split order.
+__global__ void __launch_bounds__(256)
+requant_kernel(const uint16_t* __restrict__ cache, int64_t ld_cache, int K, int group,
+               const int32_t* __restrict__ hdr, int n_slots, ExpertBits eb,
+               uint32_t* __restrict__ codes, int64_t ld_codes, uint32_t* __restrict__ sz,
+               int32_t* status) {
+  const int G = K / group;
+  const int wv = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int64_t id = static_cast<int64_t>(blockIdx.x) * 4 + wv;
+  if (id >= static_cast<int64_t>(n_slots) * G) return;  // whole waves leave together
+  const int s = static_cast<int>(id / G);
+  const int j = static_cast<int>(id % G);
+  const int bits = eb.b[hdr[2 * s]];
+  if (bits == 0) return;
+  const int per = group / 64;  // 1 or 2 values per lane
+  const uint16_t* src = cache + static_cast<int64_t>(s) * ld_cache +
+                        static_cast<int64_t>(j) * group + lane * per;
+  double v0, v1;
+  if (per == 2) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
+    v0 = fp16_to_f64(w & 0xFFFFu);
+    v1 = fp16_to_f64(w >> 16);
+  } else {
+    v0 = fp16_to_f64(*src);
+    v1 = v0;
+  }
+  double mn = v0 < v1 ? v0 : v1;
+  double mx = v0 > v1 ? v0 : v1;
+  mn = mn < 0.0 ? mn : 0.0;
+  mx = mx > 0.0 ? mx : 0.0;
+  for (int m = 1; m < 64; m <<= 1) {
+    const double a = __shfl_xor(mn, m);
+    const double b = __shfl_xor(mx, m);
+    mn = a < mn ? a : mn;
+    mx = b > mx ? b : mx;
+  }
+  const int qmax = (1 << bits) - 1;
+  const double sc = (mx - mn) / static_cast<double>(qmax);
+  const uint32_t sb = (sc == 0.0) ? 0x3C00u : fp16_ceil_bits(sc);
+  const double sf = fp16_to_f64(sb);
+  int z = static_cast<int>(rint(-mn / sf));
+  z = z < 0 ? 0 : z;
+  auto code = [&](double v) -> uint32_t {
+    double t = rint(v / sf) + static_cast<double>(z);
+    t = t < 0.0 ? 0.0 : (t > static_cast<double>(qmax) ? static_cast<double>(qmax) : t);
+    return static_cast<uint32_t>(t);
+  };
+  // word t holds codes 4t..4t+3 at bits 0, 16, 8, 24
+  const uint32_t c0 = code(v0);
+  uint32_t word;
+  if (per == 2) {  // lane l holds codes 2l (bits 0) and 2l+1 (bits 16) of the group
+    const uint32_t pair = c0 | (code(v1) << 16);
+    const uint32_t a = static_cast<uint32_t>(__shfl(static_cast<int>(pair), (2 * lane) & 63));
+    const uint32_t b = static_cast<uint32_t>(__shfl(static_cast<int>(pair), (2 * lane + 1) & 63));
+    word = a | (b << 8);
+  } else {  // lane l holds code l
+    uint32_t c[4];
+    for (int l = 0; l < 4; l++)
+      c[l] = static_cast<uint32_t>(__shfl(static_cast<int>(c0), (4 * lane + l) & 63));
+    word = c[0] | (c[1] << 16) | (c[2] << 8) | (c[3] << 24);
+  }
+  uint32_t* out = codes + static_cast<int64_t>(s) * ld_codes + static_cast<int64_t>(j) * (group / 4);
+  if (lane < group / 4) out[lane] = word;
+  if (lane == 0) {
+    sz[static_cast<int64_t>(s) * G + j] = sb | (fp16_of_small_int(z) << 16);
+    if (sb == 0x7C00u && status) *status = MOE_ERR_RANGE;
+  }
+}
+
 }  // namespace
 }  // namespace moe
 
@@ -129,6 +214,41 @@ extern "C" int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K
   hipLaunchKernelGGL(pack_kernel, dim3(static_cast<unsigned>(cdiv(total, threads))),
                      dim3(threads), 0, s, w, ld_w, K, bits, group, rows, n, codes, ld_codes,
                      sz, sz_row_stride, sz_group_stride, status);
+  return launch_status(s);
+}
+
+extern "C" int moe_requant_channels(moe_layer_t* L, int32_t kind, const uint16_t* cache,
+                                    int64_t ld_cache, const int32_t* expert_bits,
+                                    int32_t* status, void* stream) {
+  using namespace moe;
+  if (!L || kind < 0 || kind > 2 || !expert_bits) return MOE_ERR_ARG;
+  const int E = L->n_experts;
+  if (E <= 0 || E + L->n_shared > MOE_MAX_EXPERTS) return MOE_ERR_ARG;
+  if (!(L->group == 64 || L->group == 128)) return MOE_ERR_ARG;
+  const int K = kind == MOE_KIND_DOWN ? L->d_ff : L->d_model;
+  if (K <= 0 || K % L->group || K % 128) return MOE_ERR_ARG;
+  ExpertBits eb{};
+  for (int e = 0; e < E; e++) {
+    const int b = expert_bits[e];
+    if (b != 0 && !valid_bits(b)) return MOE_ERR_BITS;
+    eb.b[e] = static_cast<uint8_t>(b);
+  }
+  const moe_kind_desc_t& D = L->kind[kind];
+  if (D.n_slots < 0) return MOE_ERR_ARG;
+  if (D.n_slots == 0) return MOE_OK;
+  if (!cache || ld_cache < K || (ld_cache % 2) || (reinterpret_cast<uintptr_t>(cache) & 3u))
+    return MOE_ERR_ARG;
+  if (!D.copy_codes || !D.copy_sz || !D.copy_hdr || !D.copy_hdr_host) return MOE_ERR_ARG;
+  for (int sl = 0; sl < D.n_slots; sl++) {
+    const int e = D.copy_hdr_host[2 * sl];
+    if (e < 0 || e >= E) return MOE_ERR_SLOT;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t waves = static_cast<int64_t>(D.n_slots) * (K / L->group);
+  hipLaunchKernelGGL(requant_kernel, dim3(static_cast<unsigned>(cdiv(waves, 4))), dim3(256), 0, s,
+                     cache, ld_cache, K, L->group, D.copy_hdr, D.n_slots, eb,
+                     const_cast<uint32_t*>(D.copy_codes), code_row_words(K, 8),
+                     const_cast<uint32_t*>(D.copy_sz), status);
   return launch_status(s);
 }
 

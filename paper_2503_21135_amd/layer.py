@@ -7,7 +7,11 @@ allocator), per weight kind (gate, up, down):
              each expert's rows row-major in the packed layout of moe_quant.h,
              expert starts rounded up to 16 bytes
   sz         {fp16 scale, fp16 zero} words, group-major per expert
-  copy_*     resident 8-bit copies of the channel cache, one row per slot
+  copy_*     resident copies of the channel cache in the 8-bit code format,
+             one row per slot (8-bit codes of the original rows at load time,
+             b-bit codes after a requantization)
+  cache16    the retained original channels as binary16, one row per slot
+             (uploaded on first requantization)
   row_slot   int32 [E][R] switch table
 Plus order_gu [E][d_ff] and order_dn [E][d_model] (visiting orders rebuilt by
 the switch) and a staging buffer for the host slot list.
@@ -101,6 +105,10 @@ class MoELayer:
         if keep_status and int(self.status.item()) != 0:
             raise MoEError("moe_quant_pack reported status %d" % int(self.status.item()))
         self._bufs: Dict[int, Buffers] = {}
+        self.cache16: Dict[int, torch.Tensor] = {}
+        # precision of each routed expert's copies per kind: 0 = the 8-bit
+        # copies made at load time, b > 0 = requantized at b bits
+        self.copy_bits = {kind: np.zeros(E, np.int32) for kind in range(3)}
 
     # ------------------------------------------------------------------ packing
     def _pack_kind(self, kind: int) -> dict:
@@ -164,6 +172,36 @@ class MoELayer:
 
     def reset_switch(self) -> None:
         api.moe_set_channel_switch(self.desc, -1, None)
+
+    # ------------------------------------------------------------ requantization
+    def channel_cache(self, kind: int) -> torch.Tensor:
+        """Device float16 [n_slots][K]: the retained original channels of one
+        kind in slot order (kept in device memory, Sec. V-A)."""
+        if kind not in self.cache16:
+            c16 = np.ascontiguousarray(self.inputs.channel_cache(kind))
+            n, K = self.kinds[kind]["n_slots"], self.cfg.cols(kind, 0)
+            if c16.shape != (n, K):
+                raise MoEError("channel cache of kind %d has shape %s" % (kind, c16.shape))
+            self.cache16[kind] = torch.from_numpy(c16.view(np.float16)).to(self.device)
+        return self.cache16[kind]
+
+    def requant(self, kind: int, expert_bits, stream=None) -> None:
+        """Requantize the cached channels of one kind at each expert's new
+        precision (0 = leave the expert's copies), Sec. IV-B."""
+        eb = np.ascontiguousarray(expert_bits, np.int32)
+        api.moe_requant_channels(self.desc, kind, self.channel_cache(kind), eb,
+                                 status=self.status, stream=stream)
+        self.copy_bits[kind] = np.where(eb > 0, eb, self.copy_bits[kind]).astype(np.int32)
+
+    def switch_dataset(self, expert_bits, epoch: int = 0, stream=None) -> None:
+        """Dynamic switch for a new dataset: requantize every kind's cached
+        channels at the new per-expert precisions and install the copy-pool
+        mask of `epoch`."""
+        for kind in range(3):
+            self.requant(kind, expert_bits, stream)
+        for kind in range(3):
+            api.moe_set_channel_switch(self.desc, kind, self.inputs.slots_on(kind, epoch),
+                                       stream)
 
     # ------------------------------------------------------------------ forward
     def buffers(self, T: int) -> Buffers:

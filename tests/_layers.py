@@ -53,3 +53,25 @@ class BitsOverride:
 
     def slots_on(self, kind, epoch=0):
         return self._layer.slots_on(kind, epoch)
+
+
+class Pow2GridLayer(mi.LayerInputs):
+    """Like GridLayer, but every scale is a power of two, so each weight
+    s*(q - z) (|q - z| <= 255) is also exactly a binary16 value: quantizing the
+    binary16 rounding of a row at its expert's bit-width is still lossless."""
+
+    def weight(self, expert, kind):
+        c = self.cfg
+        R, K, g = c.rows(kind, expert), c.cols(kind, expert), c.group
+        b = int(self.bits[expert])
+        qmax = (1 << b) - 1
+        r = mi.rng(self.seed, 78, 100 + 3 * expert + kind)
+        G = K // g
+        s = 2.0 ** r.integers(-12, -6, (R, G)).astype(np.float64)
+        z = r.integers(0, qmax + 1, (R, G))
+        q = r.integers(0, qmax + 1, (R, G, g))
+        pos = np.argsort(r.random((R, G, g)), axis=2)[:, :, :2]
+        np.put_along_axis(q, pos[:, :, :1], 0, axis=2)
+        np.put_along_axis(q, pos[:, :, 1:], qmax, axis=2)
+        w = s[:, :, None] * (q - z[:, :, None])
+        return w.reshape(R, K).astype(np.float32)

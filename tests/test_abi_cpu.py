@@ -158,6 +158,29 @@ def test_switch_and_ffn_validation(lib):
     assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None) == -2
 
 
+def test_requant_validation(lib):
+    L, keep = _fake_layer()
+    rq = lib.moe_requant_channels
+
+    def eb(*b):
+        a = np.array(b, np.int32)
+        keep.append(a)
+        return a.ctypes.data_as(C.c_void_p)
+    ok = eb(8, 0, 4, 2)
+    assert rq(C.byref(L), 3, FAKE, 256, ok, None, None) == -1        # bad kind
+    assert rq(C.byref(L), 0, FAKE, 256, None, None, None) == -1      # no bit list
+    assert rq(C.byref(L), 0, FAKE, 256, eb(8, 5, 4, 2), None, None) == -2   # 5 bits
+    assert rq(C.byref(L), 0, FAKE, 200, ok, None, None) == -1        # ld_cache < K
+    assert rq(C.byref(L), 2, FAKE, 256, ok, None, None) == -1        # down: K = d_ff = 512
+    assert rq(C.byref(L), 0, FAKE, 257, ok, None, None) == -1        # odd row stride
+    assert rq(C.byref(L), 0, C.c_void_p(FAKE.value + 2), 256, ok, None, None) == -1
+    assert rq(C.byref(L), 0, None, 256, ok, None, None) == -1        # no cache
+    bad_hdr, keep2 = _fake_layer(hdr=[[4, 0], [0, 0], [0, 1], [0, 2]])
+    assert rq(C.byref(bad_hdr), 0, FAKE, 256, ok, None, None) == -5  # header expert
+    empty, keep3 = _fake_layer(n_slots=0)
+    assert rq(C.byref(empty), 0, None, 0, ok, None, None) == 0       # nothing cached
+
+
 def test_code_row_words(lib):
     # K*bits/32 words of codes plus 16 (32 at 8 bits) words of padding
     assert lib.moe_code_row_words(4096, 4) == 4096 * 4 // 32 + 16
