@@ -336,6 +336,7 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
     with itself plus 1024 decode steps of this layer, the online measure of
     the paper's overhead discussion (generation of 1024 tokens)."""
     import torch
+    import moe_inputs as mi
     from paper_2503_21135_amd import api
     cfg = layer.cfg
     for kd in range(3):
@@ -357,10 +358,22 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
         if evs:
             hip.record(evs[2], sptr)
 
-    switch(inputs.dataset_bits(reps))   # warm-up
+    # precision for each new dataset from its calibration batch: route on the
+    # GPU, then Eq. (1) and Alg. 1 on the host
+    alloc_ms, new_bits = [], []
+    for r in range(reps + 1):
+        xc, sig = mi.calibration_batch(cfg, r)
+        bc = layer.route(torch.from_numpy(xc.view(np.int16)).to("cuda:0").view(torch.bfloat16))
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        ids = bc.topk_ids.cpu().numpy()
+        s_exp, share = api.moe_expert_significance(sig, ids, cfg.n_experts)
+        new_bits.append(api.moe_allocate_bits(s_exp, share)["bits"])
+        alloc_ms.append((time.perf_counter() - w0) * 1e3)
+    switch(new_bits[reps])   # warm-up
     torch.cuda.synchronize()
     for r in range(reps):
-        eb = inputs.dataset_bits(r)
+        eb = new_bits[r]
         w0 = time.perf_counter()
         switch(eb, ev[3 * r:3 * r + 3])
         torch.cuda.synchronize()
@@ -375,9 +388,12 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
     rd = sum(n * K * 2 for n, K in zip(n_slots, Ks))
     wr = sum(n * (K + K // cfg.group * 4) for n, K in zip(n_slots, Ks))
     tot = float(np.median(rq + inst))
-    return {"workload": "%s: all cached channels of the three kinds requantized at a new "
-                        "dataset's per-expert bit-widths, then the copy mask installed"
-                        % cfg.name,
+    return {"workload": "%s: per-expert bit-widths of a new dataset from a 1024-token "
+                        "calibration batch (GPU routing, then Eq. (1) and Alg. 1 on the host), "
+                        "all cached channels of the three kinds requantized at them, then the "
+                        "copy mask installed" % cfg.name,
+            "allocation_host_ms": round(float(np.median(alloc_ms)), 4),
+            "new_bits_by_dataset": [[int(v) for v in b] for b in new_bits[:reps]],
             "cached_channels": n_slots,
             "cache_mib": round(rd / 2 ** 20, 2),
             "requant_device_ms": round(float(np.median(rq)), 4),
@@ -386,7 +402,10 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
             "host_ms": round(float(np.median(host)) * 1e3, 4),
             "requant_bytes": int(rd + wr),
             "requant_gbs": round((rd + wr) / (float(np.median(rq)) * 1e-3) / 1e9, 1),
-            "share_vs_1024_decode_steps": round(tot / (tot + 1024 * ms_step), 6)}
+            "share_vs_1024_decode_steps": round(tot / (tot + 1024 * ms_step), 6),
+            "share_with_allocation_vs_1024_decode_steps":
+                round((tot + float(np.median(alloc_ms))) /
+                      (tot + float(np.median(alloc_ms)) + 1024 * ms_step), 6)}
 
 
 def measure_bf16(layer, x, b, steps, warmup=3):

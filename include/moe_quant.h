@@ -15,6 +15,8 @@
  *   - requantization of the cached original channels at each expert's new
  *     precision when the dataset changes (Sec. IV-B "Channel Weights
  *     Requantization for New Datasets"),
+ *   - on the host, the expert significance of Eq. (1) and the precision of
+ *     each expert from Alg. 1 (Sec. III-B, Sec. IV-A),
  *   - dequantization fused with the matrix-core contraction (Sec. V-B
  *     "Channel-Grained Dequantization"), applied to the routed expert FFN.
  *
@@ -369,6 +371,56 @@ int moe_unpermute_combine(const float* o, int32_t n_split, int64_t split_stride,
                           const int32_t* inv_perm, const float* topk_w,
                           int32_t T, int32_t k, int32_t S, int32_t d,
                           float* y, void* stream);
+
+/*
+ * moe_expert_significance -- expert significance of one dataset, Eq. (1)
+ * (Sec. III-B), and each expert's token share.  Host only, no device work.
+ *
+ *   sig       host float [T]: significance of token i's combined top-K channel
+ *             output (finite, >= 0).
+ *   topk_ids  host int32 [T][k]: the experts the router chose for each token
+ *             (an expert repeated in a row counts once).
+ *   s_exp     host double [E] out: sum of sig over the tokens routed to expert
+ *             e divided by the sum over all T tokens (0 when that sum is 0);
+ *             the values add up to k.
+ *   share     host double [E] out or NULL: fraction of the T tokens routed to e.
+ * Sums run over tokens in ascending order.  MOE_ERR_ARG for an id outside
+ * [0, E), a negative or non-finite sig, k outside [1, MOE_MAX_TOPK] or E
+ * outside [1, MOE_MAX_EXPERTS].
+ */
+int moe_expert_significance(const float* sig, const int32_t* topk_ids, int32_t T,
+                            int32_t k, int32_t E, double* s_exp, double* share);
+
+/*
+ * moe_allocate_bits -- expert-level precision from significance: the fuzzy
+ * c-means of Alg. 1 (Sec. IV-A), one precision per cluster, and the
+ * low-precision-first rule for experts in the overlap of clusters.  Host only.
+ *
+ *   x, share  host double [n]: each expert's significance and token share.
+ *   levels    host int32 [c]: bit-widths from the most to the least
+ *             significant cluster, each in [1, 8] (the FFN runs {2, 3, 4, 8}).
+ *   c         clusters, 1..8 (the paper uses 4);  m > 1 fuzzifier;
+ *   eps > 0   stop when the Frobenius norm of the change of U is below eps,
+ *             or after max_iter >= 1 rounds.
+ *   alpha     membership from which an expert counts as inside a cluster.
+ *   bits      host int32 [n] out;  V host double [c], U host double [n][c] and
+ *             rounds (all optional, NULL to skip) receive the final centers,
+ *             memberships and the number of rounds.
+ * Initial U: experts sorted by ascending significance (ties by index) are cut
+ * into c consecutive runs of equal token share, each expert joining, with
+ * membership 1, the run that holds the midpoint of its own share (by rank when
+ * every share is 0).  Each round updates the centers (membership^m weighted
+ * means), then the memberships (the textbook FCM update; an expert that
+ * coincides with centers splits its membership equally among them).  The
+ * cluster with the largest center takes levels[0], the next levels[1], ...
+ * (ties by cluster index).  An expert takes the lowest precision among the
+ * clusters where its membership is >= alpha, or, if there is none, that of
+ * its largest membership (first on ties).
+ */
+int moe_allocate_bits(const double* x, const double* share, int32_t n,
+                      const int32_t* levels, int32_t c, double m, double eps,
+                      int32_t max_iter, double alpha, int32_t* bits, double* V,
+                      double* U, int32_t* rounds);
 
 /* Human-readable name of a status code. */
 const char* moe_status_str(int status);

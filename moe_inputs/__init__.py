@@ -21,6 +21,8 @@ Stream numbers:
     4000 + 1000*epoch + 3*e + kind   rows of (e, kind) switched in that epoch
     5000 + step            activations of step `step` (stress workload)
     6000 + dataset         permutation assigning bit-widths for a new dataset
+    7000 + dataset         per-token significance and activations of a
+                           dataset's calibration batch
 """
 from __future__ import annotations
 
@@ -280,6 +282,15 @@ class LayerInputs:
         if self.cfg.copies != "pool":
             return int(round(self.cfg.mask_frac * 100))
         return int(rng(self.seed, self.cfg.cfg_id, 3000 + epoch).integers(2, 11))
+
+
+def calibration_batch(cfg: LayerConfig, dataset: int, T: int = 1024, seed: int = 0):
+    """A dataset's calibration batch: bf16 activations [T][d_model] and a
+    per-token significance (exponential, mean 1) standing in for the channel
+    significance a trained model would give on real text."""
+    x = make_x(cfg, T, seed, 7000 + dataset)
+    sig = rng(seed, cfg.cfg_id, 7500 + dataset).exponential(size=T).astype(np.float32)
+    return x, sig
 
 
 def make_x(cfg: LayerConfig, T: int, seed: int = 0, stream: int = 2) -> np.ndarray:

@@ -22,6 +22,7 @@ EXPORTS = (
     "moe_ffn_plan",
     "moe_expert_ffn_mixed", "moe_expert_ffn_mixed_ev", "moe_set_channel_switch",
     "moe_requant_channels", "moe_unpermute_combine", "moe_status_str",
+    "moe_expert_significance", "moe_allocate_bits",
 )
 
 
@@ -77,6 +78,9 @@ def load() -> C.CDLL:
         "moe_requant_channels": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i64, vp, vp, vp]),
         "moe_unpermute_combine": (C.c_int, [vp, i32, i64, vp, vp, i32, i32, i32, i32, vp, vp]),
         "moe_status_str": (C.c_char_p, [C.c_int]),
+        "moe_expert_significance": (C.c_int, [vp, vp, i32, i32, i32, vp, vp]),
+        "moe_allocate_bits": (C.c_int, [vp, vp, i32, vp, i32, C.c_double, C.c_double, i32,
+                                        C.c_double, vp, vp, vp, C.POINTER(i32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)

@@ -150,3 +150,42 @@ def moe_unpermute_combine(o: torch.Tensor, n_split: int, inv_perm: torch.Tensor,
     st = load().moe_unpermute_combine(_p(o), n_split, split_stride, _p(inv_perm), _p(topk_w),
                                       T, k, S, d, _p(y), _s(stream))
     check(st, "moe_unpermute_combine")
+
+
+# ---------------------------------------------------------------------------
+# offline bit allocation (host only)
+# ---------------------------------------------------------------------------
+def _np_ptr(a: np.ndarray) -> C.c_void_p:
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def moe_expert_significance(sig: np.ndarray, topk_ids: np.ndarray, n_experts: int):
+    """Eq. (1): (s_exp float64 [E], token share float64 [E]) of one dataset."""
+    sig = np.ascontiguousarray(sig, np.float32)
+    ids = np.ascontiguousarray(topk_ids, np.int32)
+    if ids.ndim != 2 or ids.shape[0] != sig.shape[0]:
+        raise MoEError("topk_ids must be [T][k] with T = len(sig)")
+    s = np.empty(n_experts, np.float64)
+    sh = np.empty(n_experts, np.float64)
+    st = load().moe_expert_significance(_np_ptr(sig), _np_ptr(ids), ids.shape[0], ids.shape[1],
+                                        n_experts, _np_ptr(s), _np_ptr(sh))
+    check(st, "moe_expert_significance")
+    return s, sh
+
+
+def moe_allocate_bits(x: np.ndarray, share: np.ndarray, levels=(8, 4, 3, 2), m: float = 2.0,
+                      eps: float = 1e-9, max_iter: int = 300, alpha: float = 0.3) -> dict:
+    """Alg. 1 + cluster precision + low-precision-first -> per-expert bits."""
+    x = np.ascontiguousarray(x, np.float64)
+    share = np.ascontiguousarray(share, np.float64)
+    lv = np.ascontiguousarray(levels, np.int32)
+    n, c = x.shape[0], lv.shape[0]
+    bits = np.empty(n, np.int32)
+    V = np.empty(c, np.float64)
+    U = np.empty((n, c), np.float64)
+    rounds = C.c_int32(0)
+    st = load().moe_allocate_bits(_np_ptr(x), _np_ptr(share), n, _np_ptr(lv), c, m, eps,
+                                  max_iter, alpha, _np_ptr(bits), _np_ptr(V), _np_ptr(U),
+                                  C.byref(rounds))
+    check(st, "moe_allocate_bits")
+    return dict(bits=bits, V=V, U=U, rounds=int(rounds.value))

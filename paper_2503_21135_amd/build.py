@@ -21,7 +21,9 @@ FLAGS = [
 
 
 def sources() -> list:
-    return sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
+    """HIP kernel sources plus the host-only C++ of the library."""
+    return sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")) +
+                  glob.glob(os.path.join(HERE, "csrc", "*.cpp")))
 
 
 def build(verbose: bool = False) -> str:
