@@ -256,7 +256,7 @@ __device__ __forceinline__ void lds_dma16(Rsrc r, void* lds, uint32_t off, uint3
 }
 
 // ------------------------------------------------------------------ streaming kernel
-// One workgroup = 4 waves on one expert and one source class of its rows.
+// One workgroup = kWavesOf<NK> waves on one expert and one source class of its rows.
 // Each wave owns 16*RT consecutive positions of the expert's row order for
 // each of NK weight kinds (NK = 2: the gate and up rows of the same neurons;
 // NK = 1: down rows = output channels).  Within a class every kind has one
@@ -268,7 +268,11 @@ __device__ __forceinline__ void lds_dma16(Rsrc r, void* lds, uint32_t off, uint3
 // tile (NT*16 rows) are staged in LDS two groups at a time (double-buffered,
 // one barrier per two groups), so every wave reads them from LDS.
 
-constexpr int kWaves = 4;
+// Waves per workgroup: four for gate/up; eight for down, whose tile of
+// activations (h) is then shared by twice the rows (measured: the down
+// launch 7 % faster, gate/up not).
+template <int NK>
+constexpr int kWavesOf = NK == 1 ? 8 : 4;
 // Groups of codes in flight per wave: four, or two when a kind streams 8-bit
 // codes (the same bytes in flight in half the registers).  The activations
 // of chunk c+2 are loaded while chunk c is contracted, so that waiting for
@@ -279,7 +283,7 @@ template <int BG, int BU>
 constexpr int kStages = (BG == 8 || BU == 8) ? 2 : 4;
 
 // Work of one launch over experts e0 .. e0+n_e-1.  Every workgroup covers
-// kWaves*16 row positions of one source class of one expert.  Workgroups
+// kWavesOf<NK>*16 row positions of one source class of one expert.  Workgroups
 // [0, n_e*n_sw) take the switched classes (n_sw per expert, an upper bound
 // on what its copies can need; those beyond the expert's actual class sizes
 // exit at once); the rest take class 0, per_e workgroups per expert, experts
@@ -425,16 +429,17 @@ struct XTile {
 template <int NM, int NT, int RT, int NK, int BG, int BU>
 __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl, const Pre& pre, int e,
                                             int cls, int pos0, int pos1, int R, int sp, int n_split) {
+  constexpr int kThreads = 64 * kWavesOf<NK>;
   constexpr int g = NM * 32;
   constexpr int KC = XTile<NM, NT>::KC;
   constexpr int TOK = XTile<NM, NT>::TOK;
   constexpr int PIECES = TOK * KC / 8;   // 16-byte pieces per chunk
-  constexpr int PPT = PIECES / 256;
-  static_assert(PIECES % 256 == 0, "chunk must split evenly over the workgroup");
+  constexpr int PPT = (PIECES + kThreads - 1) / kThreads;
+  static_assert(PIECES % kThreads == 0 || PIECES < kThreads, "chunk must split evenly over the workgroup");
   constexpr int S = kStages<BG, BU>;
   constexpr int CG = XTile<NM, NT>::CG;
   static_assert((S == 2 || S == 4) && CG == 2, "the loop body below handles two two-group chunks");
-  static_assert(CG * TOK <= 256, "one thread per group-sum entry of a chunk");
+  static_assert(CG * TOK <= kThreads, "one thread per group-sum entry of a chunk");
   const int tid = threadIdx.x;
   const int wv = tid >> 6;
   const int lane = tid & 63;
@@ -498,12 +503,12 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   const Rsrc xsr = make_rsrc(xsum, down ? a.hsum_bytes : a.xsum_bytes);
 
   for (int t0 = seg0; t0 < seg1; t0 += TOK) {
-    // piece q = tid + 256*i of a chunk: token row q / (KC/8), column (q % (KC/8))*8
+    // piece q = tid + kThreads*i of a chunk: token row q / (KC/8), column (q % (KC/8))*8
     uint32_t arow[PPT];   // byte offset of the token's row, kOOB when absent
 #pragma unroll
     for (int i = 0; i < PPT; i++) {
-      const int p = t0 + (tid + 256 * i) / (KC / 8);
-      arow[i] = p < seg1 ? static_cast<uint32_t>(2 * (down ? h_row(a, p)
+      const int p = t0 + (tid + kThreads * i) / (KC / 8);
+      arow[i] = p < seg1 && tid + kThreads * i < PIECES ? static_cast<uint32_t>(2 * (down ? h_row(a, p)
                                                           : static_cast<int64_t>(a.perm[p]) * K))
                          : kOOB;
     }
@@ -528,7 +533,8 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
     auto write_x = [&](const u32x4 (&v)[PPT], float xsv, int buf) {
 #pragma unroll
       for (int i = 0; i < PPT; i++)
-        *reinterpret_cast<u32x4*>(&tl.x[buf][(tid + 256 * i) / (KC / 8)][acol]) = v[i];
+        if (PIECES >= kThreads || tid < PIECES)
+          *reinterpret_cast<u32x4*>(&tl.x[buf][(tid + kThreads * i) / (KC / 8)][acol]) = v[i];
       if (tid < CG * TOK) tl.xs[buf][xs_g][xs_j] = xsv;
     };
 
@@ -627,10 +633,10 @@ __device__ __forceinline__ void dispatch_class(const FfnArgs& a, XTile<NM, NT>& 
 // workgroups come first in the grid, then the class-0 workgroups, widest
 // bit-width first.
 template <int NM, int NT, int NK>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(64 * kWavesOf<NK>) __attribute__((amdgpu_waves_per_eu(2)))
 ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
   __shared__ __attribute__((aligned(16))) XTile<NM, NT> tl;
-  constexpr int rows = kWaves * 16;
+  constexpr int rows = kWavesOf<NK> * 16;
   const int wgi = blockIdx.x / n_split;
   const int sp = blockIdx.x % n_split;
   const int n_swg = map.n_e * map.n_sw;
@@ -1328,7 +1334,7 @@ int validate_layer(const moe_layer_t* L) {
 // class 1 of down at most n_down rows.
 WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
   WgMap m{};
-  constexpr int rows = kWaves * 16;
+  const int rows = (down ? kWavesOf<1> : kWavesOf<2>) * 16;
   const int E = L->n_experts;
   if (shared) {
     m.e0 = E;
@@ -1464,8 +1470,9 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     if (n_wg == 0) return;
     const dim3 grid(static_cast<unsigned>(n_wg * nsplit));
     v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, dim3(256), s, e0, e1, a, m, nsplit);
-      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, dim3(256), s, e0, e1, a, m, nsplit);
+      const dim3 block(64 * kWavesOf<NK>);
+      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, block, s, e0, e1, a, m, nsplit);
+      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, block, s, e0, e1, a, m, nsplit);
     });
   };
   using two = std::integral_constant<int, 2>;
