@@ -311,7 +311,6 @@ template <int NM, int RT, int BG, int BU>
 struct Stage {
   uint32_t cg[RT][(kWords<NM, BG>)];
   uint32_t cu[RT][(kWords<NM, BU>)];   // unused for NK = 1
-  uint32_t szw[RT][2];
 };
 
 // Source of one kind for a workgroup: resources over the expert's codes and
@@ -327,29 +326,38 @@ struct Src {
 };
 
 template <int NM, int B, int RT>
-__device__ __forceinline__ void load_kind(uint32_t (&cw)[RT][(kWords<NM, B>)], uint32_t (&szw)[RT],
-                                          const Src<RT>& s, int gi, bool gv) {
+__device__ __forceinline__ void load_kind(uint32_t (&cw)[RT][(kWords<NM, B>)], const Src<RT>& s, int gi,
+                                          bool gv) {
   constexpr uint32_t gcb = NM * 32 * B / 8;   // code bytes per row and group
   const uint32_t cadv = gv ? static_cast<uint32_t>(gi) * gcb : 0u;
-  const uint32_t sadv = gv ? static_cast<uint32_t>(gi) * s.sz_gstride : 0u;
 #pragma unroll
-  for (int rt = 0; rt < RT; rt++) {
-    bload<kWords<NM, B>>(cw[rt], s.code, gv ? s.coff[rt] : kOOB, cadv);
-    szw[rt] = __builtin_amdgcn_raw_buffer_load_b32(s.sz, gv ? s.soff[rt] : kOOB, sadv, 0);
+  for (int rt = 0; rt < RT; rt++) bload<kWords<NM, B>>(cw[rt], s.code, gv ? s.coff[rt] : kOOB, cadv);
+}
+
+// {s, z} words of the four groups [gb, gb+4): lane (r16, kq) loads row r16's
+// word of group gb + kq (zero past g1), one load per kind and row tile for
+// four groups; each group then reads its word from lane r16 + 16*(g - gb).
+template <int RT, int NK>
+__device__ __forceinline__ void load_sz4(uint32_t (&szb)[RT][2], const Src<RT> (&src)[2], int gb, int g1,
+                                         int kq) {
+  const bool ok = gb + kq < g1;
+#pragma unroll
+  for (int kk = 0; kk < NK; kk++) {
+    const uint32_t sadv = gb < g1 ? static_cast<uint32_t>(gb) * src[kk].sz_gstride : 0u;
+#pragma unroll
+    for (int rt = 0; rt < RT; rt++) {
+      const uint32_t so = src[kk].soff[rt];
+      const uint32_t voff = (ok && so != kOOB) ? so + static_cast<uint32_t>(kq) * src[kk].sz_gstride : kOOB;
+      szb[rt][kk] = __builtin_amdgcn_raw_buffer_load_b32(src[kk].sz, voff, sadv, 0);
+    }
   }
 }
 
 template <int NM, int RT, int NK, int BG, int BU>
 __device__ __forceinline__ void load_stage(Stage<NM, RT, BG, BU>& st, const Src<RT> (&src)[2], int gi,
                                            bool gv) {
-  uint32_t s0[RT], s1[RT];
-  load_kind<NM, BG, RT>(st.cg, s0, src[0], gi, gv);
-  if constexpr (NK == 2) load_kind<NM, BU, RT>(st.cu, s1, src[1], gi, gv);
-#pragma unroll
-  for (int rt = 0; rt < RT; rt++) {
-    st.szw[rt][0] = s0[rt];
-    if constexpr (NK == 2) st.szw[rt][1] = s1[rt];
-  }
+  load_kind<NM, BG, RT>(st.cg, src[0], gi, gv);
+  if constexpr (NK == 2) load_kind<NM, BU, RT>(st.cu, src[1], gi, gv);
 }
 
 // Contract one group: A fragments (activations) come from LDS.
@@ -381,16 +389,16 @@ __device__ __forceinline__ void contract_kind(const uint32_t (&cw)[(kWords<NM, B
 }
 
 template <int NM, int NT, int RT, int NK, int BG, int BU>
-__device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st,
+__device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st, const uint32_t (&szw)[RT][2],
                                               const u32x4 (&af)[NT][NM], const f32x4 (&X)[NT],
                                               uint32_t vm, uint32_t vh, f32x4 (&acc)[RT][NK][NT]) {
   f32x4 tmp[RT][NK][NT];
   float sc[RT][NK], zz[RT][NK];
 #pragma unroll
   for (int rt = 0; rt < RT; rt++) {
-    contract_kind<NM, NT, BG>(st.cg[rt], st.szw[rt][0], af, vm, vh, tmp[rt][0], sc[rt][0], zz[rt][0]);
+    contract_kind<NM, NT, BG>(st.cg[rt], szw[rt][0], af, vm, vh, tmp[rt][0], sc[rt][0], zz[rt][0]);
     if constexpr (NK == 2)
-      contract_kind<NM, NT, BU>(st.cu[rt], st.szw[rt][1], af, vm, vh, tmp[rt][1], sc[rt][1], zz[rt][1]);
+      contract_kind<NM, NT, BU>(st.cu[rt], szw[rt][1], af, vm, vh, tmp[rt][1], sc[rt][1], zz[rt][1]);
   }
   __builtin_amdgcn_sched_barrier(0);
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
@@ -554,12 +562,20 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
     for (int s = 0; s < S; s++) load_stage<NM, RT, NK, BG, BU>(st[s], src, g0 + s, g0 + s < g1);
     u32x4 vx[CG == 2 ? 2 : 1][PPT];   // activations of the next chunk(s)
     float vxs[CG == 2 ? 2 : 1];
+    uint32_t szc[RT][2], szn[RT][2];   // {s, z} words of this and the next four groups
+    load_sz4<RT, NK>(szc, src, g0, g1, kq);
     stage_x(vx[0], vxs[0], g0);
     write_x(vx[0], vxs[0], 0);
     if constexpr (CG == 2) stage_x(vx[1], vxs[1], g0 + 2);
     __syncthreads();
-    auto group = [&](Stage<NM, RT, BG, BU>& s, int buf, int gg, int gi) {
+    auto group = [&](Stage<NM, RT, BG, BU>& s, int buf, int gg, int gi, int i4) {
       if (gi < g1) {   // wave-uniform; the loads below are unconditional
+        uint32_t szw[RT][2];
+#pragma unroll
+        for (int rt = 0; rt < RT; rt++)
+#pragma unroll
+          for (int kk = 0; kk < NK; kk++)
+            szw[rt][kk] = static_cast<uint32_t>(__shfl(static_cast<int>(szc[rt][kk]), r16 + 16 * i4));
         u32x4 af[NT][NM];
         f32x4 X[NT];
 #pragma unroll
@@ -569,7 +585,7 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
             af[nt][m] = *reinterpret_cast<const u32x4*>(&tl.x[buf][nt * 16 + r16][gg * g + kq * (g / 4) + 8 * m]);
           X[nt] = *reinterpret_cast<const f32x4*>(&tl.xs[buf][gg][nt * 16 + 4 * kq]);
         }
-        compute_group<NM, NT, RT, NK, BG, BU>(s, af, X, vm, vh, acc);
+        compute_group<NM, NT, RT, NK, BG, BU>(s, szw, af, X, vm, vh, acc);
       }
       load_stage<NM, RT, NK, BG, BU>(s, src, gi + S, gi + S < g1);
     };
@@ -578,11 +594,16 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
       for (int c = 0; c < 2; c++) {   // chunk c of the iteration sits in LDS buffer c
         // vx[c] held chunk gc+2c (written to LDS already); reuse it for gc+2c+4
         stage_x(vx[c], vxs[c], gc + 2 * c + 4);
-        group(st[(2 * c) % S], c, 0, gc + 2 * c);
-        group(st[(2 * c + 1) % S], c, 1, gc + 2 * c + 1);
+        group(st[(2 * c) % S], c, 0, gc + 2 * c, 2 * c);
+        if (c == 0) load_sz4<RT, NK>(szn, src, gc + 4, g1, kq);
+        group(st[(2 * c + 1) % S], c, 1, gc + 2 * c + 1, 2 * c + 1);
         write_x(vx[c ^ 1], vxs[c ^ 1], c ^ 1);   // chunk gc+2c+2, loaded one chunk ago
         __syncthreads();
       }
+#pragma unroll
+      for (int rt = 0; rt < RT; rt++)
+#pragma unroll
+        for (int kk = 0; kk < NK; kk++) szc[rt][kk] = szn[rt][kk];
     }
 
     if constexpr (NK == 2) {
