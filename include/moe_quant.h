@@ -46,7 +46,10 @@
  * words: word 0 holds bits 0..1 of codes 0..15 and word 1 bits 0..1 of codes
  * 16..31, both in the 2-bit half-split order; word 2 holds bit 2 of codes
  * 0..31 in the 1-bit half-split order (code 2i at bit i, code 2i+1 at bit
- * 16+i).  Quantization groups run along K: group j covers codes
+ * 16+i).  For b = 6 every block of 32 codes takes six words: words 0..3 hold
+ * bits 0..3 of codes 8w..8w+7 (word w) in the 4-bit half-split order, words
+ * 4 and 5 bits 4..5 of codes 0..15 and 16..31 in the 2-bit half-split order.
+ * Quantization groups run along K: group j covers codes
  * [j*group, (j+1)*group) of a row.
  *
  * Quantizer (per row and group; Sec. IV-A, uniform quantization)
@@ -90,7 +93,7 @@ extern "C" {
 /* Status codes. */
 #define MOE_OK             0
 #define MOE_ERR_ARG       -1  /* bad size, NULL pointer or inconsistent arguments      */
-#define MOE_ERR_BITS      -2  /* bit-width outside {2, 3, 4, 8}                         */
+#define MOE_ERR_BITS      -2  /* bit-width outside {2, 3, 4, 6, 8}                      */
 #define MOE_ERR_ALIGN     -3  /* a pointer that must be 16-byte aligned is not          */
 #define MOE_ERR_WORKSPACE -4  /* workspace NULL or smaller than the size helper returns */
 #define MOE_ERR_SLOT      -5  /* switch slot out of range, duplicated, or two slots
@@ -113,7 +116,7 @@ extern "C" {
  * matrices moe_expert_ffn_mixed reads (base codes and 8-bit copies): K*bits/32
  * words of codes followed by padding of 16 words (32 words at bits == 8), so
  * that consecutive rows never start a power of two of bytes apart.  The
- * padding words are never read.  Returns 0 for bits outside {2, 3, 4, 8} or
+ * padding words are never read.  Returns 0 for bits outside {2, 3, 4, 6, 8} or
  * K not a positive multiple of 128.
  */
 int64_t moe_code_row_words(int32_t K, int32_t bits);
@@ -159,7 +162,7 @@ typedef struct moe_kind_desc {
 /*
  * One MoE layer.  Routed experts have hidden size d_ff, shared experts
  * d_ff_shared (shared experts are always applied with weight 1 and are never
- * switched).  bits[e] in {2, 3, 4, 8}; bit-width 3 needs group == 128.
+ * switched).  bits[e] in {2, 3, 4, 6, 8}; bit-widths 3 and 6 need group == 128.
  *
  * order_gu[e*d_ff + i] and order_dn[e*d_model + i] (routed experts only) are
  * the orders in which the FFN visits hidden neurons and output channels.  They
@@ -194,7 +197,7 @@ typedef struct moe_layer {
  *   w        device fp32 [R][ld_w]; the rows to quantize are rows[0..n-1]
  *            (device int32 list) or, when rows == NULL, rows 0..n-1 (n <= R).
  *   K        codes per row; K % group == 0, K % 32 == 0.
- *   bits     2, 3, 4 or 8.     group   64 or 128 (3-bit needs 128).
+ *   bits     2, 3, 4, 6 or 8.  group   64 or 128 (3- and 6-bit need 128).
  *   codes    device; list row i is written to codes[i*ld_codes ...], K*bits/32
  *            words; ld_codes >= K*bits/32; codes and ld_codes*4 16-byte aligned.
  *   sz       device; {s16, z} word of (list row i, group j) is written to
@@ -342,7 +345,7 @@ int moe_set_channel_switch(moe_layer_t* L, int32_t kind,
  *                ld_cache even and >= K): row s is the original channel named
  *                by slot s's header (copy_hdr[2s], copy_hdr[2s+1]).
  *   expert_bits  host int32 [n_experts]: new precision of each routed expert
- *                in {2, 3, 4, 8}, or 0 to leave its slots untouched; read
+ *                in {2, 3, 4, 6, 8}, or 0 to leave its slots untouched; read
  *                before the call returns.
  *   status       device int32 or NULL: set to MOE_ERR_RANGE when a scale
  *                overflows binary16 (the group is still written).
@@ -398,7 +401,7 @@ int moe_expert_significance(const float* sig, const int32_t* topk_ids, int32_t T
  *
  *   x, share  host double [n]: each expert's significance and token share.
  *   levels    host int32 [c]: bit-widths from the most to the least
- *             significant cluster, each in [1, 8] (the FFN runs {2, 3, 4, 8}).
+ *             significant cluster, each in [1, 8] (the FFN runs {2, 3, 4, 6, 8}).
  *   c         clusters, 1..8 (the paper uses 4);  m > 1 fuzzifier;
  *   eps > 0   stop when the Frobenius norm of the change of U is below eps,
  *             or after max_iter >= 1 rounds.

@@ -84,6 +84,13 @@ TINY = LayerConfig(
     d_ff=512, d_ff_shared=0, group=64, bits_literal=(8, 8, 4, 4, 4, 4, 2, 2),
     copies="all", mask_frac=0.10, outliers=4)
 
+# The small layer again with group 128 and every bit-width of the paper's
+# precision set (INT2/4/6/8) plus 3-bit.
+TINY6 = LayerConfig(
+    name="tiny-int6", cfg_id=5, d_model=256, n_experts=8, n_shared=1, top_k=2,
+    d_ff=512, d_ff_shared=256, group=128, bits_literal=(8, 6, 6, 4, 6, 3, 2, 6),
+    copies="all", mask_frac=0.10, outliers=4)
+
 MIXTRAL = LayerConfig(
     name="mixtral-8x7b", cfg_id=1, d_model=4096, n_experts=8, n_shared=0,
     top_k=2, d_ff=14336, d_ff_shared=0, group=128,
@@ -106,6 +113,7 @@ QWEN = LayerConfig(
 
 WORKLOADS: Dict[str, Workload] = {
     "tiny": Workload("tiny", TINY, 16),
+    "tiny-int6": Workload("tiny-int6", TINY6, 16),
     "mixtral-decode": Workload("mixtral-decode", MIXTRAL, 64),
     "mixtral-prefill": Workload("mixtral-prefill", MIXTRAL, 4096, zipf_s=1.1),
     "deepseek-decode": Workload("deepseek-decode", DEEPSEEK, 128),

@@ -134,7 +134,7 @@ uint16_t oracle_bf16_round(double v) {
  */
 int oracle_quantize(const float* w, int64_t ld_w, int R, int K, int bits,
                     int group, uint8_t* q, uint16_t* s16, uint16_t* z16) {
-  if (!(bits == 2 || bits == 3 || bits == 4 || bits == 8)) return ORC_ERR_BITS;
+  if (!(bits == 2 || bits == 3 || bits == 4 || bits == 6 || bits == 8)) return ORC_ERR_BITS;
   if (R < 0 || K <= 0 || group <= 0 || K % group) return ORC_ERR_ARG;
   const int qmax = (1 << bits) - 1;
   const int G = K / group;
@@ -193,14 +193,23 @@ static int halfsplit_pos(int i, int b) { return (i >> 1) * b + 16 * (i & 1); }
 /* Pack codes q[R][K] into words[R][K*bits/32] in the layout the library's
  * header defines. */
 int oracle_pack(const uint8_t* q, int R, int K, int bits, uint32_t* words) {
-  if (!(bits == 2 || bits == 3 || bits == 4 || bits == 8)) return ORC_ERR_BITS;
+  if (!(bits == 2 || bits == 3 || bits == 4 || bits == 6 || bits == 8)) return ORC_ERR_BITS;
   if (K % 32) return ORC_ERR_ARG;
   const int W = K * bits / 32;
   for (int r = 0; r < R; r++) {
     const uint8_t* qr = q + (int64_t)r * K;
     uint32_t* wr = words + (int64_t)r * W;
     memset(wr, 0, sizeof(uint32_t) * W);
-    if (bits != 3) {
+    if (bits == 6) {
+      /* per block of 32 codes: bits 0..3 of code i in word i/8 (4-bit
+       * order), bits 4..5 in word 4 + i/16 (2-bit order) */
+      for (int blk = 0; blk < K / 32; blk++)
+        for (int i = 0; i < 32; i++) {
+          uint32_t code = qr[blk * 32 + i];
+          wr[6 * blk + (i >> 3)] |= (code & 15u) << halfsplit_pos(i & 7, 4);
+          wr[6 * blk + 4 + (i >> 4)] |= (code >> 4) << halfsplit_pos(i & 15, 2);
+        }
+    } else if (bits != 3) {
       const int per = 32 / bits;
       for (int c = 0; c < K; c++)
         wr[c / per] |= (uint32_t)qr[c] << halfsplit_pos(c % per, bits);
@@ -219,13 +228,20 @@ int oracle_pack(const uint8_t* q, int R, int K, int bits, uint32_t* words) {
 
 /* Inverse of oracle_pack. */
 int oracle_unpack(const uint32_t* words, int R, int K, int bits, uint8_t* q) {
-  if (!(bits == 2 || bits == 3 || bits == 4 || bits == 8)) return ORC_ERR_BITS;
+  if (!(bits == 2 || bits == 3 || bits == 4 || bits == 6 || bits == 8)) return ORC_ERR_BITS;
   if (K % 32) return ORC_ERR_ARG;
   const int W = K * bits / 32;
   for (int r = 0; r < R; r++) {
     const uint32_t* wr = words + (int64_t)r * W;
     uint8_t* qr = q + (int64_t)r * K;
-    if (bits != 3) {
+    if (bits == 6) {
+      for (int blk = 0; blk < K / 32; blk++)
+        for (int i = 0; i < 32; i++) {
+          uint32_t lo = (wr[6 * blk + (i >> 3)] >> halfsplit_pos(i & 7, 4)) & 15u;
+          uint32_t hi = (wr[6 * blk + 4 + (i >> 4)] >> halfsplit_pos(i & 15, 2)) & 3u;
+          qr[blk * 32 + i] = (uint8_t)(lo | (hi << 4));
+        }
+    } else if (bits != 3) {
       const int per = 32 / bits;
       const uint32_t mask = (1u << bits) - 1u;
       for (int c = 0; c < K; c++)

@@ -1,6 +1,6 @@
 """MI355X (gfx950) mixed-precision MoE expert-FFN kernels: the inference hot
 path of DynaMo (arXiv 2503.21135) -- top-k routing and token permutation,
-per-expert 2/3/4/8-bit packed weights with fp16 scale/zero, the channel-level
+per-expert 2/3/4/6/8-bit packed weights with fp16 scale/zero, the channel-level
 switch to resident 8-bit copies, the fused dequant + MFMA grouped SiLU-GLU
 FFN, and un-permute/combine -- behind the C ABI of include/moe_quant.h.
 

@@ -43,7 +43,7 @@ inline int launch_status(hipStream_t s) {
   return MOE_OK;
 }
 
-inline bool valid_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 8; }
+inline bool valid_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -1,5 +1,5 @@
 // ffn.hip -- moe_expert_ffn_mixed: the routed and shared expert FFNs of one
-// MoE layer over per-expert mixed-precision packed weights (2/3/4/8-bit
+// MoE layer over per-expert mixed-precision packed weights (2/3/4/6/8-bit
 // codes, fp16 scale and zero per group of `group` inputs), with the channel
 // switch applied row by row.
 //
@@ -95,12 +95,18 @@ __device__ __forceinline__ int64_t h_row(const FfnArgs& a, int p) {
 // byte permute takes the upper halves (the bf16 patterns) of two floats.
 // 3-bit codes use two contractions: the 2-bit plane as 128 + lo and the
 // 1-bit plane as 512 + 4*hi (vh = 0x44004400, bf16 512.0, whose mantissa
-// step is 4), so the sum carries lo + 4*hi + 640.
+// step is 4), so the sum carries lo + 4*hi + 640.  6-bit codes likewise:
+// the 4-bit plane as 128 + lo and the 2-bit plane as 2048 + 16*hi
+// (vh = 0x45004500, bf16 2048.0, mantissa step 16), offset 2176.
 template <int B>
-constexpr int kPlanes = B == 3 ? 2 : 1;
+constexpr int kPlanes = (B == 3 || B == 6) ? 2 : 1;
 
 template <int B>
-constexpr float kOffset = B == 8 ? 0.f : (B == 3 ? 640.f : 128.f);
+constexpr float kOffset = B == 8 ? 0.f : (B == 3 ? 640.f : (B == 6 ? 2176.f : 128.f));
+
+// bf16 constant of the high plane of a two-plane width
+template <int BG, int BU>
+constexpr uint32_t kHighMagic = (BG == 6 || BU == 6) ? 0x45004500u : 0x44004400u;
 
 __device__ __forceinline__ uint32_t andor(uint32_t x, uint32_t mask, uint32_t vm) {
   return (x & mask) | vm;
@@ -143,6 +149,19 @@ __device__ __forceinline__ void dequant_b(const uint32_t (&cw)[NW], u32x4 (&wf)[
       const uint32_t w0 = cw[2 * m], w1 = cw[2 * m + 1];
       wf[0][m] = u32x4{pair8(ubyte_f32(w0, 0), ubyte_f32(w0, 2)), pair8(ubyte_f32(w0, 1), ubyte_f32(w0, 3)),
                        pair8(ubyte_f32(w1, 0), ubyte_f32(w1, 2)), pair8(ubyte_f32(w1, 1), ubyte_f32(w1, 3))};
+    }
+  } else if constexpr (B == 6) {  // per 32-code block: words 0-3 bits 0..3, words 4-5 bits 4..5
+    static_assert(NM % 4 == 0, "6-bit shares are whole 32-code blocks");
+#pragma unroll
+    for (int m = 0; m < NM; m++) {
+      const int blk = 6 * (m / 4);
+      const uint32_t w = cw[blk + m % 4];
+      const uint32_t h = cw[blk + 4 + (m % 4) / 2];
+      const int sh = (m & 1) * 8;
+      wf[0][m] = u32x4{andor(w, 0x000F000Fu, vm), andor(w >> 4, 0x000F000Fu, vm),
+                       andor(w >> 8, 0x000F000Fu, vm), andor(w >> 12, 0x000F000Fu, vm)};
+      wf[1][m] = u32x4{andor(h >> sh, 0x00030003u, vh), andor(h >> (sh + 2), 0x00030003u, vh),
+                       andor(h >> (sh + 4), 0x00030003u, vh), andor(h >> (sh + 6), 0x00030003u, vh)};
     }
   } else {  // 3-bit: per 32-code block, words 0/1 the 2-bit plane, word 2 the 1-bit plane
     static_assert(NM % 4 == 0, "3-bit shares are whole 32-code blocks");
@@ -205,7 +224,14 @@ __device__ __forceinline__ u32x4 bload4(Rsrc r, uint32_t off, uint32_t soff = 0)
 
 template <int NW>
 __device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off, uint32_t soff) {
-  if constexpr (NW == 16 || NW == 6) {
+  if constexpr (NW == 12) {
+#pragma unroll
+    for (int c = 0; c < 3; c++) {
+      const u32x4 a = bload4(r, off == kOOB ? kOOB : off + 16u * c, soff);
+#pragma unroll
+      for (int i = 0; i < 4; i++) cw[4 * c + i] = a[i];
+    }
+  } else if constexpr (NW == 16 || NW == 6) {
     // four 16-byte loads, or three 8-byte loads (12-byte shares are 8-byte aligned)
     constexpr int P = NW == 16 ? 4 : 2;
 #pragma unroll
@@ -246,7 +272,7 @@ __device__ __forceinline__ void bload(uint32_t (&cw)[NW], Rsrc r, uint32_t off, 
 
 // Vector-memory instructions bload<NW> issues.
 template <int NW>
-constexpr int kCodeLoads = NW == 16 ? 4 : (NW == 6 ? 3 : (NW == 8 ? 2 : 1));
+constexpr int kCodeLoads = NW == 16 ? 4 : ((NW == 6 || NW == 12) ? 3 : (NW == 8 ? 2 : 1));
 
 // Direct-to-LDS load of 16 bytes per lane: lane l of the wave writes
 // lds + 16*l (lds wave-uniform); a lane whose offset lies past the resource
@@ -273,14 +299,14 @@ __device__ __forceinline__ void lds_dma16(Rsrc r, void* lds, uint32_t off, uint3
 // launch 7 % faster, gate/up not).
 template <int NK>
 constexpr int kWavesOf = NK == 1 ? 8 : 4;
-// Groups of codes in flight per wave: four, or two when a kind streams 8-bit
-// codes (the same bytes in flight in half the registers).  The activations
+// Groups of codes in flight per wave: four, or two when a kind streams 8- or
+// 6-bit codes (about the same bytes in flight in half the registers).  The activations
 // of chunk c+2 are loaded while chunk c is contracted, so that waiting for
 // them (vector loads complete in order) never waits for a code load the loop
 // does not already need: with two-group chunks that holds for up to four
 // groups in flight.
 template <int BG, int BU>
-constexpr int kStages = (BG == 8 || BU == 8) ? 2 : 4;
+constexpr int kStages = (BG == 8 || BU == 8 || BG == 6 || BU == 6) ? 2 : 4;
 
 // Work of one launch over experts e0 .. e0+n_e-1.  Every workgroup covers
 // kWavesOf<NK>*16 row positions of one source class of one expert.  Workgroups
@@ -555,7 +581,7 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
         for (int nt = 0; nt < NT; nt++) acc[rt][kk][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // dequantization constants, kept in vector registers (see dequant_b)
-    uint32_t vm = kMagic, vh = 0x44004400u;
+    uint32_t vm = kMagic, vh = kHighMagic<BG, BU>;
     asm volatile("" : "+v"(vm), "+v"(vh));
     Stage<NM, RT, BG, BU> st[S];
 #pragma unroll
@@ -724,14 +750,20 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
       if (B == 8) dispatch_class<NM, 1, NK, 8>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
       else if (B == 4) dispatch_class<NM, 1, NK, 4>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
       else if (B == 2) dispatch_class<NM, 1, NK, 2>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
-      else if constexpr (NM == 4) dispatch_class<NM, 1, NK, 3>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      else if constexpr (NM == 4) {
+        if (B == 6) dispatch_class<NM, 1, NK, 6>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+        else dispatch_class<NM, 1, NK, 3>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      }
       return;
     }
   }
   if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
-  else if constexpr (NM == 4) dispatch_class<NM, NT, NK, 3>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  else if constexpr (NM == 4) {
+    if (B == 6) dispatch_class<NM, NT, NK, 6>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+    else dispatch_class<NM, NT, NK, 3>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  }
 }
 
 // ------------------------------------------------------------------ tile kernel
@@ -880,6 +912,14 @@ __device__ __forceinline__ u32x4 dequant_h(const uint32_t (&cw)[(kHalfWords<NM2,
     const int o = (s & 1) * 8;
 #pragma unroll
     for (int i = 0; i < 4; i++) r[i] = unpack16(w, o + 2 * i, 0x00030003u, vm);
+  } else if constexpr (B == 6) {  // per 32-code block: words 0-3 bits 0..3, words 4-5 bits 4..5
+    const int blk = 6 * (s >> 2);
+    const int q = s & 3;   // octet within the block
+    const uint32_t lo = cw[blk + q], hi = cw[blk + 4 + (q >> 1)];
+    const int o = (q & 1) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+      r[i] = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | vm;
   } else {  // 3-bit: per 32-code block words (low plane 0-15, low plane 16-31, high plane)
     const int blk = 3 * (s >> 2);
     const int q = s & 3;   // octet within the block
@@ -1207,7 +1247,10 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     if (B == 8) tile_dispatch<NM2, NK, 8>(a, tl, e, cls, pos0, pos1, R, t0, t1);
     else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
     else if (B == 2) tile_dispatch<NM2, NK, 2>(a, tl, e, cls, pos0, pos1, R, t0, t1);
-    else if constexpr (NM2 % 4 == 0) tile_dispatch<NM2, NK, 3>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if constexpr (NM2 % 4 == 0) {
+      if (B == 6) tile_dispatch<NM2, NK, 6>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+      else tile_dispatch<NM2, NK, 3>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    }
     tile_barrier();   // the LDS stages are reused by the next item
   }
 }
@@ -1331,7 +1374,7 @@ int validate_layer(const moe_layer_t* L) {
     return MOE_ERR_ARG;
   for (int e = 0; e < E + S; e++) {
     if (!valid_bits(L->bits_host[e])) return MOE_ERR_BITS;
-    if (L->bits_host[e] == 3 && L->group != 128) return MOE_ERR_ARG;
+    if ((L->bits_host[e] == 3 || L->bits_host[e] == 6) && L->group != 128) return MOE_ERR_ARG;
   }
   for (int kd = 0; kd < 3; kd++) {
     const moe_kind_desc_t& k = L->kind[kd];
@@ -1392,7 +1435,7 @@ WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
   m.n_sw = n_sw;
   for (int e = 0; e < E; e++) m.bits[e] = static_cast<int8_t>(L->bits_host[e]);
   int n = 0;
-  for (int b : {8, 4, 3, 2})
+  for (int b : {8, 6, 4, 3, 2})
     for (int e = 0; e < E; e++)
       if (L->bits_host[e] == b) m.order[n++] = static_cast<int16_t>(e);
   return m;

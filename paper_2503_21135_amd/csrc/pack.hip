@@ -84,7 +84,17 @@ pack_kernel(const float* __restrict__ w, int64_t ld_w, int K, int bits, int grou
 
   uint32_t* out = codes + static_cast<int64_t>(i) * ld_codes +
                   static_cast<int64_t>(j) * (group * bits / 32);
-  if (bits != 3) {
+  if (bits == 6) {   // per 32-code block: bits 0..3 in four 4-bit words, bits 4..5 in two 2-bit words
+    for (int blk = 0; blk < group / 32; blk++) {
+      uint32_t w[6] = {0, 0, 0, 0, 0, 0};
+      for (int l = 0; l < 32; l++) {
+        const uint32_t q = code(blk * 32 + l);
+        w[l >> 3] |= (q & 15u) << hs_pos(l & 7, 4);
+        w[4 + (l >> 4)] |= (q >> 4) << hs_pos(l & 15, 2);
+      }
+      for (int i = 0; i < 6; i++) out[6 * blk + i] = w[i];
+    }
+  } else if (bits != 3) {
     const int per = 32 / bits;
     for (int t = 0; t < group / per; t++) {
       uint32_t word = 0;
@@ -203,7 +213,7 @@ extern "C" int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K
   if (!valid_bits(bits)) return MOE_ERR_BITS;
   if (!w || !codes || !sz || R <= 0 || K <= 0 || n < 0) return MOE_ERR_ARG;
   if (!(group == 64 || group == 128) || K % group || K % 32) return MOE_ERR_ARG;
-  if (bits == 3 && group != 128) return MOE_ERR_ARG;
+  if ((bits == 3 || bits == 6) && group != 128) return MOE_ERR_ARG;
   if (ld_w < K || ld_codes < static_cast<int64_t>(K) * bits / 32) return MOE_ERR_ARG;
   if (!rows && n > R) return MOE_ERR_ARG;
   if (!aligned16(codes) || (ld_codes * 4) % 16) return MOE_ERR_ALIGN;
@@ -256,7 +266,7 @@ extern "C" const char* moe_status_str(int status) {
   switch (status) {
     case MOE_OK: return "ok";
     case MOE_ERR_ARG: return "invalid argument";
-    case MOE_ERR_BITS: return "bit-width not in {2,3,4,8}";
+    case MOE_ERR_BITS: return "bit-width not in {2,3,4,6,8}";
     case MOE_ERR_ALIGN: return "pointer or stride not 16-byte aligned";
     case MOE_ERR_WORKSPACE: return "workspace missing or too small";
     case MOE_ERR_SLOT: return "bad switch slot list";

@@ -59,6 +59,9 @@ def test_pack_validation(lib):
     assert call(g=32) == -1
     assert call(K=200) == -1
     assert call(b=3, g=64) == -1
+    assert call(b=6, g=64) == -1
+    assert call(b=7) == -2
+    assert call(b=6, g=128, ldc=47) == -1    # 6-bit rows of K = 256 need 48 words
     assert call(w=None) == -1
     assert call(ldc=8) == -1
     assert call(n=9) == -1
@@ -187,5 +190,7 @@ def test_code_row_words(lib):
     assert lib.moe_code_row_words(4096, 8) == 4096 // 4 + 32
     assert lib.moe_code_row_words(1408, 3) == 1408 * 3 // 32 + 16
     assert lib.moe_code_row_words(128, 2) == 8 + 16
+    assert lib.moe_code_row_words(4096, 6) == 4096 * 6 // 32 + 16
+    assert lib.moe_code_row_words(1408, 6) == 1408 * 6 // 32 + 16
     for K, b in ((4096, 5), (100, 4), (0, 4), (-128, 8)):
         assert lib.moe_code_row_words(K, b) == 0

@@ -178,3 +178,52 @@ def test_qwen_stress_mask_redraws(orc):
               "rel_l2", err, flush=True)
         assert err <= TOL
         assert err <= DIAG_TILE   # 512 tokens over 60 experts: the tile kernel
+
+
+@pytest.mark.parametrize("T", [16, 40, 512])
+def test_int6_layer_parity(orc, T):
+    # 6-bit experts (the paper's INT6) beside 8/4/3/2-bit ones: T = 16 and 40
+    # stream every routed expert, T = 512 tiles them; the shared 8-bit expert
+    # streams at 16 tokens and tiles beyond
+    wk, inp, layer = _layer("tiny-int6")
+    x = mi.make_x(wk.layer, T, stream=800 + T)
+    for mode in ("none", "mask", "all"):
+        if mode == "none":
+            layer.reset_switch()
+            rs = None
+        elif mode == "mask":
+            layer.set_epoch(0)
+            rs = oracle_row_slots(orc, inp)
+        else:
+            slots = {kd: np.arange(len(inp.copy_headers(kd)), dtype=np.int32) for kd in range(3)}
+            for kd in range(3):
+                layer.set_switch(kd, slots[kd])
+            rs = oracle_row_slots(orc, inp, slots=slots)
+        y, b = _run(layer, x)
+        res = orc.layer_forward(inp, x, row_slot=rs)
+        routing_matches(layer, res, b)
+        err = rel_l2(y, res["y"])
+        print("int6 T", T, mode, "rel_l2", err, flush=True)
+        assert err <= TOL
+        assert err <= (DIAG_TILE if T > 16 else DIAG_STREAM)
+
+
+def test_int6_mixtral_shaped_decode_parity(orc):
+    # full-size rows with the paper's precision set INT8/6/4/2, two experts each
+    import dataclasses
+    import paper_2503_21135_amd as P
+    cfg = dataclasses.replace(mi.MIXTRAL, name="mixtral-int2468", cfg_id=6,
+                              bit_shares=((8, 0.25), (6, 0.25), (4, 0.25), (2, 0.25)))
+    inp = mi.LayerInputs(cfg)
+    assert sorted(set(inp.bits.tolist())) == [2, 4, 6, 8]
+    layer = P.MoELayer(inp)
+    layer.set_epoch(0)
+    rs = oracle_row_slots(orc, inp)
+    x = mi.make_x(cfg, 64)
+    y, b = _run(layer, x)
+    toks = np.sort(np.random.default_rng(6).choice(64, 16, replace=False))
+    res = orc.layer_forward(inp, x, row_slot=rs, tokens=toks)
+    routing_matches(layer, res, b)
+    err = rel_l2(y[toks], res["y"])
+    print("mixtral-shaped int2/4/6/8 decode rel_l2", err, flush=True)
+    assert err <= TOL and err <= DIAG_STREAM

@@ -41,7 +41,7 @@ def _gpu_pack(w, bits, group, rows=None):
 
 
 @pytest.mark.parametrize("bits,group", [(2, 64), (4, 64), (8, 64), (2, 128), (3, 128),
-                                        (4, 128), (8, 128)])
+                                        (4, 128), (6, 128), (8, 128)])
 @pytest.mark.parametrize("kind", ["normal", "edge"])
 def test_pack_bitexact(orc, bits, group, kind):
     rng = np.random.default_rng(bits * 100 + group)

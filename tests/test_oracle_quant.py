@@ -10,13 +10,14 @@ Quantizer (Sec. IV-A, uniform quantization at the expert's precision):
       int8, written independently in numpy
   Q5  degenerate group (all zero) -> scale 1, zero 0, codes 0; overflow status
 Packer (Sec. V-B, codes packed into 32-bit words):
-  P1  hand-worked words for each bit-width
+  P1  hand-worked words for each bit-width (6-bit: the two planes checked
+      against the hand-worked 4-bit and 2-bit words)
   P2  unpack(pack(q)) == q and pack(unpack(w)) == w (bijection), sizes
 """
 import numpy as np
 import pytest
 
-BITS = (2, 3, 4, 8)
+BITS = (2, 3, 4, 6, 8)
 
 
 def np_fp16_round_up(s: float) -> np.float16:
@@ -137,6 +138,8 @@ def test_q5_degenerate_and_overflow(orc):
     assert st == orc.ERR_RANGE
     st, *_ = orc.quantize(w, 5, 128)
     assert st == orc.ERR_BITS
+    st, *_ = orc.quantize(w, 7, 128)
+    assert st == orc.ERR_BITS
 
 
 # ---------------------------------------------------------------------------
@@ -163,6 +166,13 @@ def test_p1_hand_worked_words(orc):
     q[0, 5] = 7
     q[0, 20] = 6
     assert list(orc.pack(q, 3)[0]) == [0x00300000, 0x00000020, 0x00040400]
+    # 6-bit: low four bits i % 8 and high two bits 0 (codes 0..15) or 3
+    # (codes 16..31) -> four copies of the 4-bit word above, then 0 and all ones
+    q = ((np.arange(32) % 8) + 48 * (np.arange(32) >= 16)).astype(np.uint8).reshape(1, 32)
+    assert list(orc.pack(q, 6)[0]) == [0x75316420] * 4 + [0, 0xFFFFFFFF]
+    # high two bits i % 4 -> both 2-bit words as in the 2-bit case above
+    q = (16 * (np.arange(32) % 4)).astype(np.uint8).reshape(1, 32)
+    assert list(orc.pack(q, 6)[0]) == [0] * 4 + [0xDDDD8888] * 2
 
 
 @pytest.mark.parametrize("bits", BITS)
