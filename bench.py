@@ -368,7 +368,7 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
         w0 = time.perf_counter()
         ids = bc.topk_ids.cpu().numpy()
         s_exp, share = api.moe_expert_significance(sig, ids, cfg.n_experts)
-        new_bits.append(api.moe_allocate_bits(s_exp, share)["bits"])
+        new_bits.append(api.moe_allocate_bits(s_exp, share, levels=(8, 6, 4, 2))["bits"])
         alloc_ms.append((time.perf_counter() - w0) * 1e3)
     switch(new_bits[reps])   # warm-up
     torch.cuda.synchronize()
@@ -389,7 +389,8 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
     wr = sum(n * (K + K // cfg.group * 4) for n, K in zip(n_slots, Ks))
     tot = float(np.median(rq + inst))
     return {"workload": "%s: per-expert bit-widths of a new dataset from a 1024-token "
-                        "calibration batch (GPU routing, then Eq. (1) and Alg. 1 on the host), "
+                        "calibration batch (GPU routing, then Eq. (1) and Alg. 1 on the host, "
+                        "clusters at INT8/6/4/2), "
                         "all cached channels of the three kinds requantized at them, then the "
                         "copy mask installed" % cfg.name,
             "allocation_host_ms": round(float(np.median(alloc_ms)), 4),
