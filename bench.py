@@ -409,6 +409,87 @@ def measure_dataset_switch(layer, inputs, hip, ms_step, reps=5):
                       (tot + float(np.median(alloc_ms)) + 1024 * ms_step), 6)}
 
 
+def measure_rotated(wk, layer, inputs, hip, n_copies, steps, warmup=5):
+    """The decode step rotating over n_copies independently packed copies of
+    the layer (seeds 0..n_copies-1, each with its own batch), so that no
+    copy's weights can still sit in the 256 MB Infinity Cache when its turn
+    comes again.  Gate/up GB/s from events around each gate/up launch."""
+    import ctypes as C
+    import torch
+    import moe_inputs as mi
+    import paper_2503_21135_amd as P
+    from paper_2503_21135_amd import api
+    dev = torch.device("cuda:0")
+    copies = [(layer, inputs)]
+    for r in range(1, n_copies):
+        inp = mi.LayerInputs(wk.layer, seed=r)
+        lay = P.MoELayer(inp, device="cuda:0")
+        lay.set_epoch(0)
+        copies.append((lay, inp))
+    runs = []
+    for lay, inp in copies:
+        bt = mi.make_batch(wk, inp)
+        xr = torch.from_numpy(bt.x.view(np.int16)).to(dev).view(torch.bfloat16)
+        br = None if bt.bias is None else torch.from_numpy(bt.bias).to(dev)
+        runs.append((lay, xr, br, lay.buffers(wk.tokens)))
+    ev = hip.create(2 * steps)
+
+    def step(i, evs=None):
+        lay, xr, br, b = runs[i % len(runs)]
+        lay.route(xr, br)
+        if evs is None:
+            lay.ffn(xr, b)
+        else:
+            api.moe_expert_ffn_mixed_ev(lay.desc, xr, lay.k, b.offsets, b.perm, b.o, b.ffn_ws, evs)
+        lay.combine(b)
+
+    for i in range(warmup * len(runs)):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        step(i, (C.c_void_p * 5)(None, ev[2 * i], ev[2 * i + 1], None, None))
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    gu = [hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(steps)]
+    hip.destroy(ev)
+    byt = [algorithmic_bytes(lay, b.offsets.cpu().numpy())["gate_up"] for lay, _, _, b in runs]
+    tot_b = sum(byt[i % len(runs)] for i in range(steps))
+    gbs = tot_b / (sum(gu) * 1e-3) / 1e9
+    ws_mb = round(sum(lay.packed_bytes() for lay, _, _, _ in runs) / 1e6, 1)
+    runs.clear()
+    copies.clear()
+    torch.cuda.empty_cache()
+    return {"copies": n_copies, "working_set_mb": ws_mb,
+            "ms_per_step": round(ms, 5), "tokens_per_s": round(wk.tokens / (ms * 1e-3), 1),
+            "gate_up_gbs": round(gbs, 1), "gate_up_hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def measure_copy(mib=1024, reps=10):
+    """GB/s of a plain device-to-device copy (bytes read + written), for context."""
+    import torch
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return {"bytes_moved": 2 * n * 4, "gbs": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}
+
+
 def measure_bf16(layer, x, b, steps, warmup=3):
     """Reference point for the paper's speedup claim (its only performance
     figure is quantized-vs-16-bit): the same expert FFNs with unquantized
@@ -482,6 +563,9 @@ def main():
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the companion prefill measurement of a decode workload")
     ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--rotate", type=int, default=0, metavar="N",
+                    help="also time the decode step rotating over N independently packed copies "
+                         "of the layer (defeats the Infinity Cache)")
     ap.add_argument("--no-dataset-switch", action="store_true",
                     help="skip the timing of a requantization for a new dataset")
     ap.add_argument("--no-bf16", action="store_true",
@@ -599,7 +683,11 @@ def main():
     log("gate/up %.1f GB/s %.1f TFLOP/s; FFN %.1f GB/s; %.2f TFLOP/s" %
         (achieved_gbs, achieved_tf, ffn_gbs, flops / (ffn_ms * 1e-3) / 1e12))
 
-    extra = {}
+    extra = {"copy_reference": measure_copy()}
+    log("plain copy", extra["copy_reference"])
+    if args.rotate > 1 and not wk.redraw_every:
+        extra["rotated"] = measure_rotated(wk, layer, inputs, hip, args.rotate, min(K, 100))
+        log("rotated over %d copies" % args.rotate, extra["rotated"])
     if wk.tokens <= 1024 and not wk.redraw_every:
         layer.route(x, bias)
         layer.ffn(x, b)
@@ -666,6 +754,8 @@ def main():
         "detail": {
             "host_enqueue_ms_per_step": round(enqueue / K * 1e3, 5),
             "diagnostic_step_ms": round(float(layer_ms.mean()), 5),
+            "diagnostic_step_ms_p10_p50_p90": [round(float(np.percentile(layer_ms, q)), 5)
+                                               for q in (10, 50, 90)],
             "stage_ms": {"xsum": round(float(st[0]), 5), "gate_up": round(float(st[1]), 5),
                          "hsum": round(float(st[2]), 5), "down": round(float(st[3]), 5)},
             "ffn_ms": round(ffn_ms, 5),

@@ -328,6 +328,7 @@ struct WgMap {
 struct Pre {
   int64_t code_off[2], sz_off[2];   // per kind of the launch
   int row0;                         // class 0: this lane's row of the order
+  int tt, n_tt;                     // token tile of the workgroup, when the tiles are split over workgroups
 };
 
 template <int NM, int B>
@@ -536,7 +537,11 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   const Rsrc xr = make_rsrc(down ? a.h : a.x, down ? a.h_bytes : a.x_bytes);
   const Rsrc xsr = make_rsrc(xsum, down ? a.hsum_bytes : a.xsum_bytes);
 
-  for (int t0 = seg0; t0 < seg1; t0 += TOK) {
+  // every token tile of the segment, or only tile pre.tt when the launch
+  // gives each tile its own workgroups
+  const int t_lo = seg0 + pre.tt * TOK;
+  const int t_hi = pre.n_tt > 1 ? min(t_lo + TOK, seg1) : seg1;
+  for (int t0 = t_lo; t0 < t_hi; t0 += TOK) {
     // piece q = tid + kThreads*i of a chunk: token row q / (KC/8), column (q % (KC/8))*8
     uint32_t arow[PPT];   // byte offset of the token's row, kOOB when absent
 #pragma unroll
@@ -681,11 +686,12 @@ __device__ __forceinline__ void dispatch_class(const FfnArgs& a, XTile<NM, NT>& 
 // bit-width first.
 template <int NM, int NT, int NK>
 __global__ void __launch_bounds__(64 * kWavesOf<NK>) __attribute__((amdgpu_waves_per_eu(2)))
-ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
+ffn_stream_kernel(FfnArgs a, WgMap map, int n_split, int n_tt) {
   __shared__ __attribute__((aligned(16))) XTile<NM, NT> tl;
   constexpr int rows = kWavesOf<NK> * 16;
-  const int wgi = blockIdx.x / n_split;
-  const int sp = blockIdx.x % n_split;
+  const int tt = blockIdx.x % n_tt;
+  const int wgi = blockIdx.x / n_tt / n_split;
+  const int sp = blockIdx.x / n_tt % n_split;
   const int n_swg = map.n_e * map.n_sw;
   int e, cls, blk;
   if (wgi < n_swg) {
@@ -708,6 +714,8 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split) {
 #pragma unroll
   for (int c = 0; c < 4; c++) cnt[c] = ccp[c];
   Pre pre;
+  pre.tt = tt;
+  pre.n_tt = n_tt;
 #pragma unroll
   for (int kk = 0; kk < NK; kk++) {
     pre.code_off[kk] = a.kd[kind0 + kk].code_off[e];
@@ -1317,8 +1325,13 @@ size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 struct Plan {
   int n_split;
   int nt_routed, nt_shared;   // token tiles of the streaming kernel, 0: tile kernel
+  int tt_shared;              // shared experts: workgroups per row block (one per 32-token tile), else 1
   size_t xsum_bytes, h_bytes, hsum_bytes, tile_bytes, x16_bytes, total;
 };
+
+// Shared experts with up to this many tokens stream, one workgroup set per
+// 32-token tile.
+constexpr int kSharedSplitMax = 128;
 
 // Streaming kernel for up to 28 expected tokens per expert (one or two
 // 16-token MFMA tiles, weights streamed once), tile kernel beyond.
@@ -1342,6 +1355,14 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   ns = std::min(ns, std::max(1, gmin / 8));
   p.nt_routed = pick_nt(static_cast<double>(Tk) / E);
   p.nt_shared = pick_nt(static_cast<double>(T));
+  p.tt_shared = 1;
+  if (p.nt_shared == 0 && T <= kSharedSplitMax) {
+    // shared experts at a few dozen to a hundred tokens: 32-token tiles, each
+    // on its own workgroups (the expert's weights are re-read from L2 per
+    // tile), rather than the tile kernel's few 128-token items
+    p.nt_shared = 2;
+    p.tt_shared = static_cast<int>(cdiv(T, 32));
+  }
   // split-K slices of the down projection only where the routed experts
   // stream (few tokens, too few output rows to fill the machine)
   p.n_split = p.nt_routed == 0 ? 1 : std::max(ns, 1);
@@ -1532,11 +1553,12 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     const WgMap m = stream_map(L, shared, NK == 1);
     const int64_t n_wg = static_cast<int64_t>(m.n_e) * (m.n_sw + m.per_e);
     if (n_wg == 0) return;
-    const dim3 grid(static_cast<unsigned>(n_wg * nsplit));
+    const int n_tt = shared ? p.tt_shared : 1;
+    const dim3 grid(static_cast<unsigned>(n_wg * nsplit * n_tt));
     v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
       const dim3 block(64 * kWavesOf<NK>);
-      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, block, s, e0, e1, a, m, nsplit);
-      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, block, s, e0, e1, a, m, nsplit);
+      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, block, s, e0, e1, a, m, nsplit, n_tt);
+      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, block, s, e0, e1, a, m, nsplit, n_tt);
     });
   };
   using two = std::integral_constant<int, 2>;

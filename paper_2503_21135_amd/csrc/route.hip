@@ -288,12 +288,18 @@ route_permute_fused_kernel(const int32_t* __restrict__ topk_ids, int T, int E, i
   const int c = wv;
   const int t = c * kChunk + lane;
   const bool live = t < T;
+  // the token's choices in registers: loops over j run to the compile-time
+  // bound with j < k as a predicate, so every load is issued at once and no
+  // array is indexed at run time
   int mine[MOE_MAX_TOPK];
-  for (int j = 0; j < k; j++) mine[j] = live ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++)
+    mine[j] = (live && j < k) ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
   if (c < n_chunks) {
     for (int e = 0; e < E; e++) {
       bool has = false;
-      for (int j = 0; j < k; j++) has |= (mine[j] == e);
+#pragma unroll
+      for (int j = 0; j < MOE_MAX_TOPK; j++) has |= (mine[j] == e);
       const uint64_t m = __ballot(has);
       if (lane == 0) cb[c * E + e] = __popcll(m);
     }
@@ -342,22 +348,28 @@ route_permute_fused_kernel(const int32_t* __restrict__ topk_ids, int T, int E, i
   for (int s2 = threadIdx.x; s2 <= S; s2 += blockDim.x) offsets[E + s2] = routed + s2 * T;
   if (c >= n_chunks) return;
   int pos[MOE_MAX_TOPK];
-  for (int j = 0; j < k; j++) pos[j] = -1;
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++) pos[j] = -1;
   for (int e = 0; e < E; e++) {
     bool has = false;
-    for (int j = 0; j < k; j++) has |= (mine[j] == e);
+#pragma unroll
+    for (int j = 0; j < MOE_MAX_TOPK; j++) has |= (mine[j] == e);
     const uint64_t m = __ballot(has);
     if (has) {
       const int p = seg[e] + cb[c * E + e] + __popcll(m & below);
-      for (int j = 0; j < k; j++)
+#pragma unroll
+      for (int j = 0; j < MOE_MAX_TOPK; j++)
         if (mine[j] == e) pos[j] = p;
     }
   }
   if (!live) return;
   const int64_t row = static_cast<int64_t>(t) * (k + S);
-  for (int j = 0; j < k; j++) {
-    perm_token[pos[j]] = t;
-    inv_perm[row + j] = pos[j];
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++) {
+    if (j < k) {
+      perm_token[pos[j]] = t;
+      inv_perm[row + j] = pos[j];
+    }
   }
   for (int s2 = 0; s2 < S; s2++) {
     const int p = routed + s2 * T + t;
