@@ -537,11 +537,9 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   const Rsrc xr = make_rsrc(down ? a.h : a.x, down ? a.h_bytes : a.x_bytes);
   const Rsrc xsr = make_rsrc(xsum, down ? a.hsum_bytes : a.xsum_bytes);
 
-  // every token tile of the segment, or only tile pre.tt when the launch
-  // gives each tile its own workgroups
-  const int t_lo = seg0 + pre.tt * TOK;
-  const int t_hi = pre.n_tt > 1 ? min(t_lo + TOK, seg1) : seg1;
-  for (int t0 = t_lo; t0 < t_hi; t0 += TOK) {
+  // token tiles pre.tt, pre.tt + n_tt, ... of the segment (all of them
+  // when the launch has one workgroup set per row block)
+  for (int t0 = seg0 + pre.tt * TOK; t0 < seg1; t0 += pre.n_tt * TOK) {
     // piece q = tid + kThreads*i of a chunk: token row q / (KC/8), column (q % (KC/8))*8
     uint32_t arow[PPT];   // byte offset of the token's row, kOOB when absent
 #pragma unroll
@@ -1325,13 +1323,17 @@ size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 struct Plan {
   int n_split;
   int nt_routed, nt_shared;   // token tiles of the streaming kernel, 0: tile kernel
-  int tt_shared;              // shared experts: workgroups per row block (one per 32-token tile), else 1
+  int tt_routed, tt_shared;   // workgroup sets per row block, each taking every n-th 32-token tile
   size_t xsum_bytes, h_bytes, hsum_bytes, tile_bytes, x16_bytes, total;
 };
 
 // Shared experts with up to this many tokens stream, one workgroup set per
-// 32-token tile.
-constexpr int kSharedSplitMax = 128;
+// 32-token tile (measured on the Qwen-shaped layer, 512 tokens: step 440 ->
+// 389 us against the tile kernel's few items).
+constexpr int kSharedSplitMax = 512;
+// Routed experts expecting up to this many tokens stream too, with
+// workgroup sets taking every n_tt-th 32-token tile of the expert.
+constexpr int kRoutedSplitMax = 96;
 
 // Streaming kernel for up to 28 expected tokens per expert (one or two
 // 16-token MFMA tiles, weights streamed once), tile kernel beyond.
@@ -1354,6 +1356,13 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   ns = std::min(ns, 8);
   ns = std::min(ns, std::max(1, gmin / 8));
   p.nt_routed = pick_nt(static_cast<double>(Tk) / E);
+  p.tt_routed = 1;
+  if (p.nt_routed == 0 && Tk <= static_cast<int64_t>(kRoutedSplitMax) * E) {
+    // a few dozen tokens per expert: 32-token tiles over several workgroup
+    // sets (one more than the mean needs, for skewed loads)
+    p.nt_routed = 2;
+    p.tt_routed = static_cast<int>(cdiv(cdiv(Tk, E), 32)) + 1;
+  }
   p.nt_shared = pick_nt(static_cast<double>(T));
   p.tt_shared = 1;
   if (p.nt_shared == 0 && T <= kSharedSplitMax) {
@@ -1553,7 +1562,7 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     const WgMap m = stream_map(L, shared, NK == 1);
     const int64_t n_wg = static_cast<int64_t>(m.n_e) * (m.n_sw + m.per_e);
     if (n_wg == 0) return;
-    const int n_tt = shared ? p.tt_shared : 1;
+    const int n_tt = shared ? p.tt_shared : p.tt_routed;
     const dim3 grid(static_cast<unsigned>(n_wg * nsplit * n_tt));
     v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
       const dim3 block(64 * kWavesOf<NK>);

@@ -227,3 +227,23 @@ def test_int6_mixtral_shaped_decode_parity(orc):
     err = rel_l2(y[toks], res["y"])
     print("mixtral-shaped int2/4/6/8 decode rel_l2", err, flush=True)
     assert err <= TOL and err <= DIAG_STREAM
+
+
+def test_routed_token_tiles_split_skewed(orc):
+    # 200 tokens, top-2 of 8 experts: 50 expected per expert, so the routed
+    # experts stream with their 32-token tiles spread over three workgroup
+    # sets; the bias piles most tokens on experts 0 and 1 (seven tiles each)
+    # and leaves experts 5 and 6 empty
+    wk, inp, layer = _layer("tiny")
+    layer.set_epoch(0)
+    rs = oracle_row_slots(orc, inp)
+    x = mi.make_x(wk.layer, 200, stream=950)
+    bias = np.array([40, 40, 0, 0, 0, -40, -40, 1], np.float32)
+    y, b = _run(layer, x, bias)
+    res = orc.layer_forward(inp, x, bias=bias, row_slot=rs)
+    routing_matches(layer, res, b)
+    loads = np.diff(res["offsets"])[:8]
+    assert loads[0] > 150 and loads[1] > 150 and loads[5] == 0 and loads[6] == 0
+    err = rel_l2(y, res["y"])
+    print("routed tile split, loads", loads.tolist(), "rel_l2", err, flush=True)
+    assert err <= TOL and err <= DIAG_STREAM
