@@ -247,3 +247,28 @@ def test_routed_token_tiles_split_skewed(orc):
     err = rel_l2(y, res["y"])
     print("routed tile split, loads", loads.tolist(), "rel_l2", err, flush=True)
     assert err <= TOL and err <= DIAG_STREAM
+
+
+def test_tile_sets_with_split_k(orc):
+    # 4 routed experts (8/4/6/2-bit) + 1 shared, d_ff = 2048, 64 tokens: the
+    # routed experts expect 32 tokens and the shared one sees 64, so both
+    # stream over two workgroup sets of 32-token tiles, and the down
+    # projection is split over K (two slices summed by the combine)
+    import dataclasses
+    import paper_2503_21135_amd as P
+    cfg = dataclasses.replace(mi.TINY6, name="tile-sets", cfg_id=7, n_experts=4, n_shared=1,
+                              d_ff=2048, d_ff_shared=2048, bits_literal=(8, 4, 6, 2))
+    inp = mi.LayerInputs(cfg)
+    layer = P.MoELayer(inp)
+    from paper_2503_21135_amd import api
+    n_split, _ = api.moe_ffn_plan(layer.desc, 64, cfg.top_k)
+    assert n_split == 2
+    layer.set_epoch(0)
+    rs = oracle_row_slots(orc, inp)
+    x = mi.make_x(cfg, 64, stream=960)
+    y, b = _run(layer, x)
+    res = orc.layer_forward(inp, x, row_slot=rs)
+    routing_matches(layer, res, b)
+    err = rel_l2(y, res["y"])
+    print("tile sets + split-K loads", np.diff(res["offsets"]).tolist(), "rel_l2", err, flush=True)
+    assert err <= TOL and err <= DIAG_STREAM
