@@ -9,7 +9,6 @@
 // requantized.  The visiting order of rows (order_gu / order_dn) is rebuilt
 // as a stable partition by precision source, which keeps most 16-row tiles of
 // the FFN uniform in bit-width.
-#include <unordered_set>
 #include <vector>
 
 #include "common.hpp"
@@ -117,9 +116,11 @@ extern "C" int moe_set_channel_switch(moe_layer_t* L, int32_t kind, const int32_
     if (n_on < 0 || n_on > K.n_slots) return MOE_ERR_SLOT;
     if (n_on > 0 && (!slots_on || !K.copy_hdr || !K.copy_hdr_host || !L->staging))
       return MOE_ERR_ARG;
-    std::vector<char> seen(static_cast<size_t>(K.n_slots), 0);
-    std::unordered_set<int64_t> rows;
-    rows.reserve(static_cast<size_t>(n_on) * 2);
+    // duplicate slots and two slots on one (expert, row): one flag per slot
+    // and one per row of the kind (E*R bytes, reused across calls)
+    static thread_local std::vector<uint8_t> seen, rows;
+    seen.assign(static_cast<size_t>(K.n_slots), 0);
+    rows.assign(static_cast<size_t>(E) * R, 0);
     for (int i = 0; i < n_on; i++) {
       const int sl = slots_on[i];
       if (sl < 0 || sl >= K.n_slots || seen[sl]) return MOE_ERR_SLOT;
@@ -127,7 +128,9 @@ extern "C" int moe_set_channel_switch(moe_layer_t* L, int32_t kind, const int32_
       const int e = K.copy_hdr_host[2 * sl];
       const int r = K.copy_hdr_host[2 * sl + 1];
       if (e < 0 || e >= E || r < 0 || r >= R) return MOE_ERR_SLOT;
-      if (!rows.insert(static_cast<int64_t>(e) * R + r).second) return MOE_ERR_SLOT;
+      uint8_t& f = rows[static_cast<size_t>(e) * R + r];
+      if (f) return MOE_ERR_SLOT;
+      f = 1;
     }
     if (n_on > 0 &&
         hipMemcpyAsync(L->staging, slots_on, sizeof(int32_t) * n_on, hipMemcpyHostToDevice, s) !=
