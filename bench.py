@@ -162,19 +162,38 @@ def cpu_baseline(wk, inputs, batch, min_seconds):
     W = [oracle.effective_weight(inputs.weight(e, kd), int(inputs.bits[e]), cfg.group,
                                  np.nonzero(rs[kd][e] >= 0)[0]) for kd in (0, 1, 2)]
     rows = perm[off[e]:off[e + 1]]
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        _, ids, _ = oracle.route(batch.x, inputs.router, k, batch.bias)
-        oracle.permute(ids, cfg.n_experts, cfg.n_shared)
-        oracle.expert_ffn(W[0], W[1], W[2], batch.x, rows)
-        reps += 1
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
+
+    def run(seconds):
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            _, ids, _ = oracle.route(batch.x, inputs.router, k, batch.bias)
+            oracle.permute(ids, cfg.n_experts, cfg.n_shared)
+            oracle.expert_ffn(W[0], W[1], W[2], batch.x, rows)
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= seconds:
+                return reps, dt
+
+    threads = oracle.num_threads()
+    reps, dt = run(min_seconds)
     tok = reps * len(rows) / k
-    return {"value": round(tok / dt, 4), "unit": "tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+    # the same sample on one thread, a quarter as long
+    oracle.set_num_threads(1)
+    reps1, dt1 = run(min_seconds / 4)
+    oracle.set_num_threads(threads)
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": round(tok / dt, 4), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle", "cpu": model,
+            "value_1_thread": round(reps1 * len(rows) / k / dt1, 4),
             "sample": "%d x (route+permute of all %d tokens, fp64 FFN of the %d rows of "
                       "expert %d at %d bits, %d%% of rows switched); %d expert rows = "
                       "%.1f tokens at top-%d in %.1f s"

@@ -68,6 +68,7 @@ def lib():
             "oracle_expert_ffn": (None, [vp, vp, vp, i32, i32, vp, vp, i32, i32, vp]),
             "oracle_combine": (None, [vp, vp, vp, i32, i32, i32, i32, vp]),
             "oracle_num_threads": (i32, []),
+            "oracle_set_num_threads": (None, [i32]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -79,6 +80,11 @@ def lib():
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's later OpenMP loops (timing only)."""
+    lib().oracle_set_num_threads(int(n))
 
 
 # ---------------------------------------------------------------------------

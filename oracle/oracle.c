@@ -40,6 +40,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Sets the threads of later OpenMP loops (n >= 1); for timing only. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* 16-bit float formats, written from the IEEE 754 definitions.             */
 /* ------------------------------------------------------------------------ */
