@@ -69,10 +69,11 @@
  * even) before the down projection, as the paper feeds 16-bit activations to
  * the matrix cores (Sec. V-B); accumulation is fp32.  The weights enter in
  * one of two ways, chosen per launch from the expected tokens per expert:
- *   - few tokens (decode): exactly -- the matrix cores multiply the integer
+ *   - up to 96 expected tokens per routed expert, and shared experts over up
+ *     to 512 tokens (decode): exactly -- the matrix cores multiply the integer
  *     codes (exact in bf16) by the bf16 activations, and each group's scale
  *     and zero point are applied to the fp32 partial sum;
- *   - many tokens (prefill, shared experts): as the 16-bit dequantized
+ *   - more tokens (prefill): as the 16-bit dequantized
  *     operand of the paper (Sec. V-B), fp16(s * (q - z)) -- one rounding per
  *     weight -- multiplied by fp16 copies of the activations and of h.  The
  *     bf16 values convert to fp16 exactly while |value| < 65504; larger

@@ -1336,7 +1336,9 @@ constexpr int kSharedSplitMax = 512;
 constexpr int kRoutedSplitMax = 96;
 
 // Streaming kernel for up to 28 expected tokens per expert (one or two
-// 16-token MFMA tiles, weights streamed once), tile kernel beyond.
+// 16-token MFMA tiles, weights streamed once); beyond, make_plan spreads the
+// 32-token tiles of mid-sized experts over workgroup sets, and the rest go to
+// the tile kernel.
 int pick_nt(double tokens) {
   if (tokens <= 12.0) return 1;
   if (tokens <= 28.0) return 2;
@@ -1366,9 +1368,9 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   p.nt_shared = pick_nt(static_cast<double>(T));
   p.tt_shared = 1;
   if (p.nt_shared == 0 && T <= kSharedSplitMax) {
-    // shared experts at a few dozen to a hundred tokens: 32-token tiles, each
-    // on its own workgroups (the expert's weights are re-read from L2 per
-    // tile), rather than the tile kernel's few 128-token items
+    // shared experts at a few dozen to a few hundred tokens: 32-token tiles,
+    // each on its own workgroups (the expert's weights are re-read from L2
+    // per tile), rather than the tile kernel's few 128-token items
     p.nt_shared = 2;
     p.tt_shared = static_cast<int>(cdiv(T, 32));
   }

@@ -9,8 +9,8 @@ the method's arithmetic (h in bf16).  Two kernels compute the FFN:
 - the streaming kernel (experts with few tokens) contracts the exact
   weights, so its error is fp32 accumulation order plus rare one-ulp flips
   of h: diagnostic bound 5e-4 where every row streams (measured 1e-5..2e-4);
-- the tile kernel (experts with many tokens, e.g. shared experts or
-  prefill) rounds each dequantized weight to fp16, the paper's 16-bit
+- the tile kernel (experts with many tokens: prefill, or shared experts
+  over more than 512 tokens) rounds each dequantized weight to fp16, the paper's 16-bit
   dequantized operand; the relative error of ~2e-4 per weight flips h's
   bf16 rounding more often: diagnostic bound 1.5e-3 (measured 1.0e-3 ..
   1.2e-3, the CPU study of fp16-rounded weights predicts 1.0e-3..1.1e-3).
@@ -123,8 +123,9 @@ def _sampled_parity(orc, name, n_tok, seed=0):
 
 
 def test_deepseek_decode_parity(orc):
-    # routed experts stream; the two shared experts see all 128 tokens and tile
-    assert _sampled_parity(orc, "deepseek-decode", 48) <= DIAG_TILE
+    # routed experts stream; the two shared experts see all 128 tokens and
+    # stream too, their four 32-token tiles on separate workgroup sets
+    assert _sampled_parity(orc, "deepseek-decode", 48) <= DIAG_STREAM
 
 
 def test_mixtral_decode_parity(orc):
@@ -177,14 +178,14 @@ def test_qwen_stress_mask_redraws(orc):
         print("qwen step", step, "epoch", epoch, "switched %d%%" % inp.switch_percent(epoch),
               "rel_l2", err, flush=True)
         assert err <= TOL
-        assert err <= DIAG_TILE   # 512 tokens over 60 experts: the tile kernel
+        assert err <= DIAG_STREAM   # ~34 tokens per routed expert, 512 on the shared one: all streamed
 
 
 @pytest.mark.parametrize("T", [16, 40, 512])
 def test_int6_layer_parity(orc, T):
     # 6-bit experts (the paper's INT6) beside 8/4/3/2-bit ones: T = 16 and 40
     # stream every routed expert, T = 512 tiles them; the shared 8-bit expert
-    # streams at 16 tokens and tiles beyond
+    # streams (over 32-token tile sets from 40 tokens on)
     wk, inp, layer = _layer("tiny-int6")
     x = mi.make_x(wk.layer, T, stream=800 + T)
     for mode in ("none", "mask", "all"):
@@ -205,7 +206,7 @@ def test_int6_layer_parity(orc, T):
         err = rel_l2(y, res["y"])
         print("int6 T", T, mode, "rel_l2", err, flush=True)
         assert err <= TOL
-        assert err <= (DIAG_TILE if T > 16 else DIAG_STREAM)
+        assert err <= (DIAG_TILE if T > 40 else DIAG_STREAM)
 
 
 def test_int6_mixtral_shaped_decode_parity(orc):
