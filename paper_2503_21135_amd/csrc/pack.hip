@@ -126,8 +126,13 @@ struct ExpertBits {
   uint8_t b[MOE_MAX_EXPERTS];
 };
 
-// One wave per (copy slot, group).  Lane l holds group/64 consecutive fp16
-// values of the cached row; the range, scale, zero and codes follow the same
+// Groups per wave of the requantization: their loads are all issued before
+// the first group is reduced.
+constexpr int kRqGroups = 4;
+
+// One wave per (copy slot, kRqGroups groups).  Lane l holds group/64
+// consecutive fp16 values of each group of the cached row; the range, scale,
+// zero and codes follow the same
 // binary64 quantizer as pack_kernel, so a row requantized at b bits carries
 // exactly the codes moe_quant_pack gives for its binary16 values.  The b-bit
 // codes are stored in the 8-bit copy format: each byte holds one code, bytes
@@ -138,66 +143,71 @@ requant_kernel(const uint16_t* __restrict__ cache, int64_t ld_cache, int K, int 
                uint32_t* __restrict__ codes, int64_t ld_codes, uint32_t* __restrict__ sz,
                int32_t* status) {
   const int G = K / group;
+  const int GB = (G + kRqGroups - 1) / kRqGroups;
   const int wv = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int64_t id = static_cast<int64_t>(blockIdx.x) * 4 + wv;
-  if (id >= static_cast<int64_t>(n_slots) * G) return;  // whole waves leave together
-  const int s = static_cast<int>(id / G);
-  const int j = static_cast<int>(id % G);
+  if (id >= static_cast<int64_t>(n_slots) * GB) return;  // whole waves leave together
+  const int s = static_cast<int>(id / GB);
+  const int j0 = static_cast<int>(id % GB) * kRqGroups;
   const int bits = eb.b[hdr[2 * s]];
   if (bits == 0) return;
   const int per = group / 64;  // 1 or 2 values per lane
-  const uint16_t* src = cache + static_cast<int64_t>(s) * ld_cache +
-                        static_cast<int64_t>(j) * group + lane * per;
-  double v0, v1;
-  if (per == 2) {
-    const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
-    v0 = fp16_to_f64(w & 0xFFFFu);
-    v1 = fp16_to_f64(w >> 16);
-  } else {
-    v0 = fp16_to_f64(*src);
-    v1 = v0;
+  const uint16_t* row = cache + static_cast<int64_t>(s) * ld_cache + lane * per;
+  uint32_t raw[kRqGroups];
+#pragma unroll
+  for (int q = 0; q < kRqGroups; q++) {
+    const uint16_t* src = row + static_cast<int64_t>(j0 + q) * group;
+    raw[q] = j0 + q >= G ? 0u
+                         : (per == 2 ? *reinterpret_cast<const uint32_t*>(src) : static_cast<uint32_t>(*src));
   }
-  double mn = v0 < v1 ? v0 : v1;
-  double mx = v0 > v1 ? v0 : v1;
-  mn = mn < 0.0 ? mn : 0.0;
-  mx = mx > 0.0 ? mx : 0.0;
-  for (int m = 1; m < 64; m <<= 1) {
-    const double a = __shfl_xor(mn, m);
-    const double b = __shfl_xor(mx, m);
-    mn = a < mn ? a : mn;
-    mx = b > mx ? b : mx;
-  }
-  const int qmax = (1 << bits) - 1;
-  const double sc = (mx - mn) / static_cast<double>(qmax);
-  const uint32_t sb = (sc == 0.0) ? 0x3C00u : fp16_ceil_bits(sc);
-  const double sf = fp16_to_f64(sb);
-  int z = static_cast<int>(rint(-mn / sf));
-  z = z < 0 ? 0 : z;
-  auto code = [&](double v) -> uint32_t {
-    double t = rint(v / sf) + static_cast<double>(z);
-    t = t < 0.0 ? 0.0 : (t > static_cast<double>(qmax) ? static_cast<double>(qmax) : t);
-    return static_cast<uint32_t>(t);
-  };
-  // word t holds codes 4t..4t+3 at bits 0, 16, 8, 24
-  const uint32_t c0 = code(v0);
-  uint32_t word;
-  if (per == 2) {  // lane l holds codes 2l (bits 0) and 2l+1 (bits 16) of the group
-    const uint32_t pair = c0 | (code(v1) << 16);
-    const uint32_t a = static_cast<uint32_t>(__shfl(static_cast<int>(pair), (2 * lane) & 63));
-    const uint32_t b = static_cast<uint32_t>(__shfl(static_cast<int>(pair), (2 * lane + 1) & 63));
-    word = a | (b << 8);
-  } else {  // lane l holds code l
-    uint32_t c[4];
-    for (int l = 0; l < 4; l++)
-      c[l] = static_cast<uint32_t>(__shfl(static_cast<int>(c0), (4 * lane + l) & 63));
-    word = c[0] | (c[1] << 16) | (c[2] << 8) | (c[3] << 24);
-  }
-  uint32_t* out = codes + static_cast<int64_t>(s) * ld_codes + static_cast<int64_t>(j) * (group / 4);
-  if (lane < group / 4) out[lane] = word;
-  if (lane == 0) {
-    sz[static_cast<int64_t>(s) * G + j] = sb | (fp16_of_small_int(z) << 16);
-    if (sb == 0x7C00u && status) *status = MOE_ERR_RANGE;
+#pragma unroll
+  for (int q = 0; q < kRqGroups; q++) {
+    const int j = j0 + q;
+    if (j >= G) break;   // wave-uniform
+    const double v0 = fp16_to_f64(raw[q] & 0xFFFFu);
+    const double v1 = per == 2 ? fp16_to_f64(raw[q] >> 16) : v0;
+    double mn = v0 < v1 ? v0 : v1;
+    double mx = v0 > v1 ? v0 : v1;
+    mn = mn < 0.0 ? mn : 0.0;
+    mx = mx > 0.0 ? mx : 0.0;
+    for (int m = 1; m < 64; m <<= 1) {
+      const double a = __shfl_xor(mn, m);
+      const double b = __shfl_xor(mx, m);
+      mn = a < mn ? a : mn;
+      mx = b > mx ? b : mx;
+    }
+    const int qmax = (1 << bits) - 1;
+    const double sc = (mx - mn) / static_cast<double>(qmax);
+    const uint32_t sb = (sc == 0.0) ? 0x3C00u : fp16_ceil_bits(sc);
+    const double sf = fp16_to_f64(sb);
+    int z = static_cast<int>(rint(-mn / sf));
+    z = z < 0 ? 0 : z;
+    auto code = [&](double v) -> uint32_t {
+      double t = rint(v / sf) + static_cast<double>(z);
+      t = t < 0.0 ? 0.0 : (t > static_cast<double>(qmax) ? static_cast<double>(qmax) : t);
+      return static_cast<uint32_t>(t);
+    };
+    // word t holds codes 4t..4t+3 at bits 0, 16, 8, 24
+    const uint32_t c0 = code(v0);
+    uint32_t word;
+    if (per == 2) {  // lane l holds codes 2l (bits 0) and 2l+1 (bits 16) of the group
+      const uint32_t pair = c0 | (code(v1) << 16);
+      const uint32_t a = static_cast<uint32_t>(__shfl(static_cast<int>(pair), (2 * lane) & 63));
+      const uint32_t b = static_cast<uint32_t>(__shfl(static_cast<int>(pair), (2 * lane + 1) & 63));
+      word = a | (b << 8);
+    } else {  // lane l holds code l
+      uint32_t c[4];
+      for (int l = 0; l < 4; l++)
+        c[l] = static_cast<uint32_t>(__shfl(static_cast<int>(c0), (4 * lane + l) & 63));
+      word = c[0] | (c[1] << 16) | (c[2] << 8) | (c[3] << 24);
+    }
+    uint32_t* out = codes + static_cast<int64_t>(s) * ld_codes + static_cast<int64_t>(j) * (group / 4);
+    if (lane < group / 4) out[lane] = word;
+    if (lane == 0) {
+      sz[static_cast<int64_t>(s) * G + j] = sb | (fp16_of_small_int(z) << 16);
+      if (sb == 0x7C00u && status) *status = MOE_ERR_RANGE;
+    }
   }
 }
 
@@ -254,7 +264,7 @@ extern "C" int moe_requant_channels(moe_layer_t* L, int32_t kind, const uint16_t
     if (e < 0 || e >= E) return MOE_ERR_SLOT;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t waves = static_cast<int64_t>(D.n_slots) * (K / L->group);
+  const int64_t waves = static_cast<int64_t>(D.n_slots) * cdiv(K / L->group, kRqGroups);
   hipLaunchKernelGGL(requant_kernel, dim3(static_cast<unsigned>(cdiv(waves, 4))), dim3(256), 0, s,
                      cache, ld_cache, K, L->group, D.copy_hdr, D.n_slots, eb,
                      const_cast<uint32_t*>(D.copy_codes), code_row_words(K, 8),
