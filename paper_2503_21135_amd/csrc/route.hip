@@ -273,19 +273,22 @@ constexpr int kFusedChunks = 16; // token chunks the fused path holds in LDS
 // Histogram, scans and stable scatter of up to kFusedChunks chunks in one
 // workgroup (batches of up to 1024 tokens).  The segment order is the same as
 // the three-kernel path's: experts ascending, then tokens ascending, shared
-// experts last.
+// experts last.  Each chunk keeps one 64-bit lane mask per expert (bit l set
+// when token l of the chunk chose the expert), so a count is a popcount and a
+// token's rank among the chunk's rows of an expert is the popcount of the mask
+// below its lane: no thread loops over the experts.
 __global__ void __launch_bounds__(kPermWaves * kWave)
 route_permute_fused_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k, int S,
                            int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token,
                            int32_t* __restrict__ inv_perm) {
-  __shared__ int32_t cb[kFusedChunks * MOE_MAX_EXPERTS];  // chunk counts, then chunk bases
-  __shared__ int32_t seg[MOE_MAX_EXPERTS + 1];            // segment offsets, then the total
+  __shared__ uint64_t mask[kFusedChunks * MOE_MAX_EXPERTS];  // per chunk and expert
+  __shared__ int32_t cb[kFusedChunks * MOE_MAX_EXPERTS];     // chunk bases per expert
+  __shared__ int32_t seg[MOE_MAX_EXPERTS + 1];               // segment offsets, then the total
   const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
   const int n_chunks = (T + kChunk - 1) / kChunk;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   // wave c holds chunk c (n_chunks <= kPermWaves) and keeps its choices
-  const int c = wv;
+  const int c = threadIdx.x >> 6;
   const int t = c * kChunk + lane;
   const bool live = t < T;
   // the token's choices in registers: loops over j run to the compile-time
@@ -295,30 +298,25 @@ route_permute_fused_kernel(const int32_t* __restrict__ topk_ids, int T, int E, i
 #pragma unroll
   for (int j = 0; j < MOE_MAX_TOPK; j++)
     mine[j] = (live && j < k) ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
-  if (c < n_chunks) {
-    for (int e = 0; e < E; e++) {
-      bool has = false;
-#pragma unroll
-      for (int j = 0; j < MOE_MAX_TOPK; j++) has |= (mine[j] == e);
-      const uint64_t m = __ballot(has);
-      if (lane == 0) cb[c * E + e] = __popcll(m);
-    }
-  }
+  for (int i = threadIdx.x; i < n_chunks * E; i += blockDim.x) mask[i] = 0;
   __syncthreads();
-  // per expert: exclusive scan over the chunks
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++)
+    if (mine[j] >= 0) atomicOr(&mask[c * E + mine[j]], 1ull << lane);
+  __syncthreads();
+  // per expert: exclusive scan of the chunk counts
   if (threadIdx.x < E) {
     const int e = threadIdx.x;
     int run = 0;
     for (int cc = 0; cc < n_chunks; cc++) {
-      const int v = cb[cc * E + e];
       cb[cc * E + e] = run;
-      run += v;
+      run += __popcll(mask[cc * E + e]);
     }
     seg[e] = run;
   }
   __syncthreads();
   // exclusive scan of the segment sizes over experts: four per lane of wave 0
-  if (wv == 0) {
+  if (c == 0) {
     int v[4];
     int sum = 0;
 #pragma unroll
@@ -346,29 +344,15 @@ route_permute_fused_kernel(const int32_t* __restrict__ topk_ids, int T, int E, i
   const int routed = seg[MOE_MAX_EXPERTS];
   for (int e = threadIdx.x; e < E; e += blockDim.x) offsets[e] = seg[e];
   for (int s2 = threadIdx.x; s2 <= S; s2 += blockDim.x) offsets[E + s2] = routed + s2 * T;
-  if (c >= n_chunks) return;
-  int pos[MOE_MAX_TOPK];
-#pragma unroll
-  for (int j = 0; j < MOE_MAX_TOPK; j++) pos[j] = -1;
-  for (int e = 0; e < E; e++) {
-    bool has = false;
-#pragma unroll
-    for (int j = 0; j < MOE_MAX_TOPK; j++) has |= (mine[j] == e);
-    const uint64_t m = __ballot(has);
-    if (has) {
-      const int p = seg[e] + cb[c * E + e] + __popcll(m & below);
-#pragma unroll
-      for (int j = 0; j < MOE_MAX_TOPK; j++)
-        if (mine[j] == e) pos[j] = p;
-    }
-  }
   if (!live) return;
   const int64_t row = static_cast<int64_t>(t) * (k + S);
 #pragma unroll
   for (int j = 0; j < MOE_MAX_TOPK; j++) {
     if (j < k) {
-      perm_token[pos[j]] = t;
-      inv_perm[row + j] = pos[j];
+      const int i = c * E + mine[j];
+      const int p = seg[mine[j]] + cb[i] + __popcll(mask[i] & below);
+      perm_token[p] = t;
+      inv_perm[row + j] = p;
     }
   }
   for (int s2 = 0; s2 < S; s2++) {
