@@ -6,7 +6,8 @@
 // a histogram of expert choices, an exclusive scan into segment offsets and a
 // stable scatter of token indices.  Everything is bitwise reproducible: the
 // logit reduction order is fixed (moe_quant.h), the exponential is the
-// library's own, and the permutation uses no atomics.
+// library's own, and the permutation's only atomics are bitwise ORs, whose
+// result does not depend on their order.
 #include "common.hpp"
 
 #pragma clang fp contract(off)
