@@ -1163,7 +1163,10 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
 template <int NM2, int NK, int B>
 __device__ __forceinline__ void tile_dispatch(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0,
                                               int pos1, int R, int t0, int t1) {
-  const int wv = threadIdx.x >> 6;
+  // the wave index through readfirstlane: the kind, the class bit and the
+  // buffer descriptors chosen by them are then scalar values, so no load is
+  // wrapped in a loop over the distinct descriptors of the wave's lanes
+  const int wv = uni(static_cast<int>(threadIdx.x >> 6));
   const int kk = NK == 2 ? wv / 4 : 0;
   const int rb = NK == 2 ? wv % 4 : wv;
   const bool copy = (cls >> kk) & 1;
