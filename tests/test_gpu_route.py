@@ -93,3 +93,13 @@ def test_route_run_to_run(orc):
     b = gpu_route(batch.x, inp.router, None, 6, 2)
     for key in a:
         assert np.array_equal(a[key], b[key])
+
+
+def test_route_empty_batch():
+    # no tokens: every segment (routed and shared) is empty, nothing is read
+    rng = np.random.default_rng(5)
+    d, E, k, S = 256, 8, 2, 1
+    x = np.zeros((0, d), np.uint16)
+    router = (rng.standard_normal((E, d)) * 0.02).astype(np.float32)
+    g = gpu_route(x, router, None, k, S)
+    assert np.array_equal(g["off"], np.zeros(E + S + 1, np.int32))
