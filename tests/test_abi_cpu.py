@@ -155,6 +155,9 @@ def test_switch_and_ffn_validation(lib):
     L.d_ff = 500
     assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None) == -1
     L.d_ff = 512
+    # an empty batch: OK without touching any buffer (null activations, no workspace)
+    assert f(C.byref(L), None, 0, 2, None, None, None, None, 0, None) == 0
+    assert f(C.byref(L), None, -1, 2, None, None, None, None, 0, None) == -1
     bits = np.array([8, 4, 5, 2], np.int32)
     keep.append(bits)
     L.bits_host = bits.ctypes.data
