@@ -185,34 +185,56 @@ route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __r
   }
 }
 
+// One chunk's expert lane masks in LDS: bit l of mask[e] is set when token
+// l of the chunk chose expert e (one LDS atomic OR per choice; OR does not
+// depend on the order of the atomics).  The token's choices stay in
+// registers, j < k a predicate of the compile-time loop.
+__device__ __forceinline__ void chunk_masks(const int32_t* __restrict__ topk_ids, int T, int E, int k,
+                                            int c, int lane, uint64_t* mask, int (&mine)[MOE_MAX_TOPK]) {
+  const int t = c * kChunk + lane;
+  const bool live = t < T;
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++)
+    mine[j] = (live && j < k) ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
+  for (int e = lane; e < E; e += kWave) mask[e] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++)
+    if (mine[j] >= 0) atomicOr(&mask[mine[j]], 1ull << lane);
+  __syncthreads();
+}
+
 // hist[c][e] = number of tokens of chunk c that selected e.
 __global__ void __launch_bounds__(64)
 route_hist_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k,
                   int32_t* __restrict__ hist) {
+  __shared__ uint64_t mask[MOE_MAX_EXPERTS];
   const int c = blockIdx.x;
   const int lane = threadIdx.x;
-  const int t = c * kChunk + lane;
   int mine[MOE_MAX_TOPK];
-  for (int j = 0; j < k; j++) mine[j] = (t < T) ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
-  for (int e = 0; e < E; e++) {
-    bool has = false;
-    for (int j = 0; j < k; j++) has |= (mine[j] == e);
-    const uint64_t m = __ballot(has);
-    if (lane == 0) hist[static_cast<int64_t>(c) * E + e] = __popcll(m);
-  }
+  chunk_masks(topk_ids, T, E, k, c, lane, mask, mine);
+  for (int e = lane; e < E; e += kWave) hist[static_cast<int64_t>(c) * E + e] = __popcll(mask[e]);
 }
 
 // offsets[] and per-chunk segment bases (single workgroup; one thread per
-// expert column, chunks in order).
+// expert column, chunks in order, their counts loaded 16 at a time).
 __global__ void __launch_bounds__(256)
 route_scan_kernel(const int32_t* __restrict__ hist, int n_chunks, int T, int E, int k, int S,
                   int32_t* __restrict__ base, int32_t* __restrict__ offsets) {
   __shared__ int32_t tot[MOE_MAX_EXPERTS];
+  constexpr int kBatch = 16;
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
     int s = 0;
-    for (int c = 0; c < n_chunks; c++) {
-      base[static_cast<int64_t>(c) * E + e] = s;
-      s += hist[static_cast<int64_t>(c) * E + e];
+    for (int c0 = 0; c0 < n_chunks; c0 += kBatch) {
+      int v[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; i++)
+        v[i] = c0 + i < n_chunks ? hist[static_cast<int64_t>(c0 + i) * E + e] : 0;
+#pragma unroll
+      for (int i = 0; i < kBatch; i++) {
+        if (c0 + i < n_chunks) base[static_cast<int64_t>(c0 + i) * E + e] = s;
+        s += v[i];
+      }
     }
     tot[e] = s;
   }
@@ -228,38 +250,29 @@ route_scan_kernel(const int32_t* __restrict__ hist, int n_chunks, int T, int E, 
 }
 
 // Stable scatter: rank of a token inside its chunk's share of segment e is
-// the number of earlier lanes of the chunk that selected e.
+// the number of earlier lanes of the chunk that selected e, the popcount of
+// the chunk's mask of e below the lane.
 __global__ void __launch_bounds__(64)
 route_scatter_kernel(const int32_t* __restrict__ topk_ids, int T, int E, int k, int S,
                      const int32_t* __restrict__ base, const int32_t* __restrict__ offsets,
                      int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_perm) {
+  __shared__ uint64_t mask[MOE_MAX_EXPERTS];
   const int c = blockIdx.x;
   const int lane = threadIdx.x;
   const int t = c * kChunk + lane;
-  const bool live = t < T;
   int mine[MOE_MAX_TOPK];
-  int pos[MOE_MAX_TOPK];
-  for (int j = 0; j < k; j++) {
-    mine[j] = live ? topk_ids[static_cast<int64_t>(t) * k + j] : -1;
-    pos[j] = -1;
-  }
+  chunk_masks(topk_ids, T, E, k, c, lane, mask, mine);
+  if (t >= T) return;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int e = 0; e < E; e++) {
-    bool has = false;
-    for (int j = 0; j < k; j++) has |= (mine[j] == e);
-    const uint64_t m = __ballot(has);
-    if (!m) continue;
-    if (has) {
-      const int p = offsets[e] + base[static_cast<int64_t>(c) * E + e] + __popcll(m & below);
-      for (int j = 0; j < k; j++)
-        if (mine[j] == e) pos[j] = p;
-    }
-  }
-  if (!live) return;
   const int64_t row = static_cast<int64_t>(t) * (k + S);
-  for (int j = 0; j < k; j++) {
-    perm_token[pos[j]] = t;
-    inv_perm[row + j] = pos[j];
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_TOPK; j++) {
+    if (j < k) {
+      const int e = mine[j];
+      const int p = offsets[e] + base[static_cast<int64_t>(c) * E + e] + __popcll(mask[e] & below);
+      perm_token[p] = t;
+      inv_perm[row + j] = p;
+    }
   }
   for (int s = 0; s < S; s++) {
     const int p = offsets[E + s] + t;
