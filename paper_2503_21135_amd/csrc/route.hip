@@ -92,51 +92,18 @@ __device__ __forceinline__ void router_partials(const uint16_t* __restrict__ xr,
   }
 }
 
-// One workgroup (8 waves) per token.  Wave w owns experts w, w + 8, ... and
-// computes their logits four, two or one at a time; wave 0 then selects the
-// top k and forms the weights.
-__global__ void __launch_bounds__(kRouteWaves * kWave)
-route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
-                  const float* __restrict__ bias, int E, int k,
-                  int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
-  __shared__ float lgs[MOE_MAX_EXPERTS];
-  const int t = blockIdx.x;
-  const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
-  const uint16_t* xr = x + static_cast<int64_t>(t) * d;
-  const int mine = wv < E ? (E - 1 - wv) / kRouteWaves + 1 : 0;  // experts of this wave
-  auto finish = [&](int e, float acc) {
-    float v = tree_sum(acc);
-    if (bias) v = v + bias[e];
-    if (lane == 0) lgs[e] = v;
-  };
-  int m = 0;
-  for (; m + 4 <= mine; m += 4) {
-    float acc[4];
-    router_partials<4, 32>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
-#pragma unroll
-    for (int j = 0; j < 4; j++) finish(wv + (m + j) * kRouteWaves, acc[j]);
-  }
-  if (m + 2 <= mine) {
-    float acc[2];
-    router_partials<2, 32>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
-#pragma unroll
-    for (int j = 0; j < 2; j++) finish(wv + (m + j) * kRouteWaves, acc[j]);
-    m += 2;
-  }
-  if (m < mine) {
-    float acc[1];
-    router_partials<1, 64>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
-    finish(wv + m * kRouteWaves, acc[0]);
-  }
-  __syncthreads();
-  if (wv != 0) return;
+// Top k of one token's E logits src[0 .. E) by (logit desc, index asc) and
+// the softmax over the selected logits; one wave, every lane ends with the
+// same picks, lane 0 writes the token's row of topk_ids / topk_w.
+__device__ __forceinline__ void select_topk(const float* src, int E, int k, int t, int lane,
+                                            int32_t* __restrict__ topk_ids,
+                                            float* __restrict__ topk_w) {
   constexpr int kMaxPer = MOE_MAX_EXPERTS / kWave;
   float lg[kMaxPer];
 #pragma unroll
   for (int m = 0; m < kMaxPer; m++) {
     const int e = m * kWave + lane;
-    lg[m] = e < E ? lgs[e] : -INFINITY;
+    lg[m] = e < E ? src[e] : -INFINITY;
   }
   // top-k by (logit desc, index asc); every lane ends with the same picks
   bool taken[kMaxPer];
@@ -183,6 +150,123 @@ route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __r
       topk_w[static_cast<int64_t>(t) * k + j] = ex[j] / S;
     }
   }
+}
+
+// One workgroup (8 waves) per token.  Wave w owns experts w, w + 8, ... and
+// computes their logits four, two or one at a time; wave 0 then selects the
+// top k and forms the weights.
+__global__ void __launch_bounds__(kRouteWaves * kWave)
+route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
+                  const float* __restrict__ bias, int E, int k,
+                  int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
+  __shared__ float lgs[MOE_MAX_EXPERTS];
+  const int t = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const uint16_t* xr = x + static_cast<int64_t>(t) * d;
+  const int mine = wv < E ? (E - 1 - wv) / kRouteWaves + 1 : 0;  // experts of this wave
+  auto finish = [&](int e, float acc) {
+    float v = tree_sum(acc);
+    if (bias) v = v + bias[e];
+    if (lane == 0) lgs[e] = v;
+  };
+  int m = 0;
+  for (; m + 4 <= mine; m += 4) {
+    float acc[4];
+    router_partials<4, 32>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
+#pragma unroll
+    for (int j = 0; j < 4; j++) finish(wv + (m + j) * kRouteWaves, acc[j]);
+  }
+  if (m + 2 <= mine) {
+    float acc[2];
+    router_partials<2, 32>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
+#pragma unroll
+    for (int j = 0; j < 2; j++) finish(wv + (m + j) * kRouteWaves, acc[j]);
+    m += 2;
+  }
+  if (m < mine) {
+    float acc[1];
+    router_partials<1, 64>(xr, wr, d, wv + m * kRouteWaves, kRouteWaves, lane, acc);
+    finish(wv + m * kRouteWaves, acc[0]);
+  }
+  __syncthreads();
+  if (wv != 0) return;
+  select_topk(lgs, E, k, t, lane, topk_ids, topk_w);
+}
+
+constexpr int kLogitWaves = 4;      // waves of a logits workgroup
+constexpr int kLogitExperts = 8;    // experts of a logits workgroup, two per wave
+constexpr int kLogitTokens = 8;     // tokens of a logits workgroup
+constexpr int kSplitRouterMinT = 1024;
+
+// Router logits of large batches with the experts spread over workgroups:
+// workgroup (token block, expert block) computes 8 tokens x 8 experts, wave w
+// experts 2w, 2w + 1 of the block, so a CU reads a slice of the router
+// matrix once for 8 tokens instead of the whole matrix per token.  Each
+// logit is the header's sum: lane l adds columns l, l + 64, ... in ascending
+// order with one FMA each, then the halving tree over the lanes, then the
+// bias.
+template <int TB, int RB>
+__global__ void __launch_bounds__(kLogitWaves * kWave)
+route_logits_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
+                    const float* __restrict__ bias, int E, float* __restrict__ logits) {
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int t0 = blockIdx.x * TB;
+  const int e0 = blockIdx.y * kLogitExperts + 2 * wv;
+  if (e0 >= E) return;   // wave-uniform; no barrier follows
+  int er[2], tr[TB];
+#pragma unroll
+  for (int j = 0; j < 2; j++) er[j] = min(e0 + j, E - 1);   // clamped rows are computed, not stored
+#pragma unroll
+  for (int tb = 0; tb < TB; tb++) tr[tb] = min(t0 + tb, T - 1);
+  float acc[TB][2];
+#pragma unroll
+  for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+    for (int j = 0; j < 2; j++) acc[tb][j] = 0.0f;
+  for (int c0 = 0; c0 < d; c0 += kWave * RB) {
+    float w[2][RB];
+    uint32_t xb[TB][RB];
+#pragma unroll
+    for (int i = 0; i < RB; i++) {
+      if (c0 + kWave * i < d) {   // uniform: d is a multiple of 64
+        const int c = c0 + kWave * i + lane;
+#pragma unroll
+        for (int j = 0; j < 2; j++) w[j][i] = wr[static_cast<int64_t>(er[j]) * d + c];
+#pragma unroll
+        for (int tb = 0; tb < TB; tb++) xb[tb][i] = x[static_cast<int64_t>(tr[tb]) * d + c];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < RB; i++) {
+      if (c0 + kWave * i < d) {
+#pragma unroll
+        for (int tb = 0; tb < TB; tb++) {
+          const float xv = __uint_as_float(xb[tb][i] << 16);
+#pragma unroll
+          for (int j = 0; j < 2; j++) acc[tb][j] = __fmaf_rn(xv, w[j][i], acc[tb][j]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      float v = tree_sum(acc[tb][j]);
+      if (bias) v = v + bias[er[j]];
+      if (lane == 0 && t0 + tb < T && e0 + j < E) logits[static_cast<int64_t>(t0 + tb) * E + e0 + j] = v;
+    }
+}
+
+// Top k and weights of the logits rows, one wave per token.
+__global__ void __launch_bounds__(4 * kWave)
+route_select_kernel(const float* __restrict__ logits, int T, int E, int k,
+                    int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  select_topk(logits + static_cast<int64_t>(t) * E, E, k, t, threadIdx.x & 63, topk_ids, topk_w);
 }
 
 // One chunk's expert lane masks in LDS: bit l of mask[e] is set when token
@@ -399,7 +483,9 @@ extern "C" size_t moe_route_workspace_bytes(int32_t T, int32_t E, int32_t k, int
   (void)S;
   if (T < 0 || E <= 0) return 0;
   const size_t n_chunks = static_cast<size_t>((T + moe::kChunk - 1) / moe::kChunk);
-  return 2 * moe::align256(sizeof(int32_t) * (n_chunks > 0 ? n_chunks : 1) * E);
+  // chunk histogram, chunk bases, then the logits [T][E] of large batches
+  const size_t logits = T >= moe::kSplitRouterMinT ? sizeof(float) * static_cast<size_t>(T) * E : 0;
+  return 2 * moe::align256(sizeof(int32_t) * (n_chunks > 0 ? n_chunks : 1) * E) + moe::align256(logits);
 }
 
 extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const float* w_router,
@@ -418,11 +504,22 @@ extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const 
   if (!ws || ws_bytes < need) return MOE_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int n_chunks = static_cast<int>(cdiv(T, kChunk));
+  const size_t half = align256(sizeof(int32_t) * static_cast<size_t>(n_chunks > 0 ? n_chunks : 1) * E);
   int32_t* hist = static_cast<int32_t*>(ws);
-  int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + need / 2);
-  if (T > 0)
+  int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + half);
+  if (T >= kSplitRouterMinT) {
+    // large batches: logits over (8-token, 8-expert) workgroups, then the top
+    // k per token (the second launch costs more than it saves on small ones)
+    float* logits = reinterpret_cast<float*>(static_cast<char*>(ws) + 2 * half);
+    hipLaunchKernelGGL((route_logits_kernel<kLogitTokens, 16>),
+                       dim3(static_cast<unsigned>(cdiv(T, kLogitTokens)), static_cast<unsigned>(cdiv(E, kLogitExperts))),
+                       dim3(kLogitWaves * kWave), 0, s, x, T, d, w_router, bias, E, logits);
+    hipLaunchKernelGGL(route_select_kernel, dim3(static_cast<unsigned>(cdiv(T, 4))), dim3(4 * kWave), 0, s,
+                       logits, T, E, k, topk_ids, topk_w);
+  } else if (T > 0) {
     hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(T)), dim3(kRouteWaves * kWave),
                        0, s, x, T, d, w_router, bias, E, k, topk_ids, topk_w);
+  }
   if (n_chunks <= kFusedChunks) {
     hipLaunchKernelGGL(route_permute_fused_kernel, dim3(1), dim3(kPermWaves * kWave), 0, s,
                        topk_ids, T, E, k, S, offsets, perm_token, inv_perm);
