@@ -197,7 +197,7 @@ route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __r
 constexpr int kLogitWaves = 4;      // waves of a logits workgroup
 constexpr int kLogitExperts = 8;    // experts of a logits workgroup, two per wave
 constexpr int kLogitTokens = 8;     // tokens of a logits workgroup
-constexpr int kSplitRouterMinT = 1024;
+constexpr int kSplitRouterMinT = 256;
 
 // Router logits of large batches with the experts spread over workgroups:
 // workgroup (token block, expert block) computes 8 tokens x 8 experts, wave w
