@@ -70,7 +70,7 @@ struct FfnArgs {
   int64_t split_stride;
   int n_split_out;     // slices of o the combine adds (tile launches zero the others)
   int32_t* tile_prefix;   // workspace: 4 x (MOE_MAX_EXPERTS + 1) item prefixes
-  const uint16_t* x16;  // [rows][d] fp16 copies of the gathered x rows (tile kernel)
+  const uint16_t* x16;  // [T][d] fp16 copy of x (tile kernel; row of permuted row p: perm[p])
   uint32_t x_bytes, h_bytes, xsum_bytes, hsum_bytes, x16_bytes;   // resource sizes (< 2^31)
   uint32_t copy_bytes[3], copy_sz_bytes[3];
   int E, S, d, f, fs, group;
@@ -1048,7 +1048,7 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
     const int c = (sl % SPT) ^ (t % SPT);
     const int p = t0 + t;
     aoff[i] = (sl < SL && p < t1)
-                  ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(p) * K) + 16 * c)
+                  ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(a.perm[p]) * K) + 16 * c)
                   : kOOB;
   }
   auto stage_a = [&](int buf, int gi) {
@@ -1301,16 +1301,18 @@ group_sum_kernel(FfnArgs a, const uint16_t* __restrict__ in, const int32_t* __re
   if (live && q == 0) out[static_cast<int64_t>(j) * a.rows + p] = s;
 }
 
-// x16[p][c] = fp16(x[perm[p]][c]) for permuted rows p0 <= p < p1, the
-// activation operand of the tile kernel (exact for |x| < 65504, the bf16
-// values being a subset of fp16's in that range); 8 values per thread.
-__global__ void __launch_bounds__(256) gather_f16_kernel(FfnArgs a, int p0, int p1) {
+// x16[t][c] = fp16(x[t][c]) for the T tokens, the activation operand of the
+// tile kernel, which reaches the row of permuted row p through perm[p] (one
+// copy per token instead of one per routed and shared row; exact for
+// |x| < 65504, the bf16 values being a subset of fp16's in that range); 8
+// values per thread.
+__global__ void __launch_bounds__(256) gather_f16_kernel(FfnArgs a, int T) {
   const int per_row = a.d / 8;
   const int64_t id = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (id >= static_cast<int64_t>(p1 - p0) * per_row) return;
-  const int p = p0 + static_cast<int>(id / per_row);
+  if (id >= static_cast<int64_t>(T) * per_row) return;
+  const int p = static_cast<int>(id / per_row);
   const int c = static_cast<int>(id % per_row) * 8;
-  const u32x4 v = *reinterpret_cast<const u32x4*>(a.x + static_cast<int64_t>(a.perm[p]) * a.d + c);
+  const u32x4 v = *reinterpret_cast<const u32x4*>(a.x + static_cast<int64_t>(p) * a.d + c);
   u32x4 o;
 #pragma unroll
   for (int i = 0; i < 4; i++) {
@@ -1386,7 +1388,7 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   p.hsum_bytes = align256(sizeof(float) * static_cast<size_t>(rows) * (fmax / g));
   p.tile_bytes = align256(sizeof(int32_t) * 4 * (MOE_MAX_EXPERTS + 1));
   const bool tiled = p.nt_routed == 0 || (S > 0 && p.nt_shared == 0);
-  p.x16_bytes = tiled ? align256(sizeof(uint16_t) * static_cast<size_t>(rows) * L->d_model) : 0;
+  p.x16_bytes = tiled ? align256(sizeof(uint16_t) * static_cast<size_t>(T) * L->d_model) : 0;
   p.total = p.xsum_bytes + p.h_bytes + p.hsum_bytes + p.tile_bytes + p.x16_bytes + 256;
   return p;
 }
@@ -1530,12 +1532,15 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   std::vector<Launch> xsum, gate_up, hsum, down;
   // activation preparation per row range: group sums [d/g][rows] for the
   // streaming kernel, fp16 copies for the tile kernel
+  bool x16_done = false;
   auto prep = [&](int p0, int p1, bool tiled) {
     if (p1 <= p0) return;
-    if (tiled) {
-      const int64_t n = static_cast<int64_t>(p1 - p0) * (a.d / 8);
+    if (tiled) {   // one fp16 copy of the T token rows serves every tiled range
+      if (x16_done) return;
+      x16_done = true;
+      const int64_t n = static_cast<int64_t>(T) * (a.d / 8);
       xsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-        klaunch(gather_f16_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1, a, p0, p1);
+        klaunch(gather_f16_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1, a, T);
       });
     } else {
       const int64_t n = static_cast<int64_t>(p1 - p0) * (a.d / g) * (g / 8);
