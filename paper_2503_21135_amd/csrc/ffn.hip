@@ -1268,18 +1268,20 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
 // out[j * rows + p] = sum over group j of the bf16 row of permuted row p, in
 // fp32: each of g/8 lanes adds its 8 values in order, then an xor tree over
 // those lanes.  The row of p starts at perm[p] * ld (gathered activations)
-// or, with perm == NULL, at h_row(p) (hidden activations, K = that row's
-// width).  Consecutive lane groups take consecutive p so the stores coalesce.
+// or, with perm == NULL, at h_row(p) (hidden activations).  Rows p < p_split
+// have K columns, the others K2 (routed and shared hidden rows in one
+// launch); groups past a row's width are skipped.  Consecutive lane groups
+// take consecutive p so the stores coalesce.
 template <int NM>
 __global__ void __launch_bounds__(256)
 group_sum_kernel(FfnArgs a, const uint16_t* __restrict__ in, const int32_t* __restrict__ perm,
-                 int64_t ld, int p0, int p1, int K, float* __restrict__ out) {
+                 int64_t ld, int p0, int p1, int K, int p_split, int K2, float* __restrict__ out) {
   constexpr int g = NM * 32;
   constexpr int lanes = g / 8;
-  const int G = K / g;
+  const int G = max(K, K2) / g;
   const int64_t id = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t n = static_cast<int64_t>(p1 - p0) * G * lanes;
-  const bool live = id < n;
+  bool live = id < n;
   const int64_t item = id / lanes;
   const int q = static_cast<int>(id % lanes);
   const int np = p1 - p0;
@@ -1288,6 +1290,9 @@ group_sum_kernel(FfnArgs a, const uint16_t* __restrict__ in, const int32_t* __re
   if (live) {
     j = static_cast<int>(item / np);
     p = p0 + static_cast<int>(item % np);
+    live = j < (p < p_split ? K : K2) / g;   // the same for every lane of the item
+  }
+  if (live) {
     const int64_t row = perm ? static_cast<int64_t>(perm[p]) * ld : h_row(a, p);
     const u32x4 v = *reinterpret_cast<const u32x4*>(in + row + static_cast<int64_t>(j) * g + q * 8);
 #pragma unroll
@@ -1546,12 +1551,16 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
       const int64_t n = static_cast<int64_t>(p1 - p0) * (a.d / g) * (g / 8);
       xsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
         klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
-                a, a.x, a.perm, static_cast<int64_t>(a.d), p0, p1, a.d, const_cast<float*>(a.xsum));
+                a, a.x, a.perm, static_cast<int64_t>(a.d), p0, p1, a.d, p1, a.d, const_cast<float*>(a.xsum));
       });
     }
   };
-  prep(0, a.Tk, p.nt_routed == 0);
-  if (S > 0) prep(a.Tk, a.rows, p.nt_shared == 0);
+  if (p.nt_routed != 0 && (S == 0 || p.nt_shared != 0)) {
+    prep(0, a.rows, false);   // every row streams: one launch of group sums
+  } else {
+    prep(0, a.Tk, p.nt_routed == 0);
+    if (S > 0) prep(a.Tk, a.rows, p.nt_shared == 0);
+  }
   int32_t* prefix = a.tile_prefix;
   auto add = [&](std::vector<Launch>& v, auto nk, bool shared, int nt, int nsplit) {
     constexpr int NK = decltype(nk)::value;
@@ -1585,21 +1594,19 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   add(gate_up, two{}, false, p.nt_routed, 1);
   if (S > 0) add(gate_up, two{}, true, p.nt_shared, 1);
   {  // group sums of h, [max(f,fs)/g][rows], for the rows the streaming kernel reads
-    const int64_t n = p.nt_routed != 0 ? static_cast<int64_t>(a.Tk) * (a.f / g) * (g / 8) : 0;
-    if (n > 0)
+    // (routed rows f wide, shared rows fs wide; one launch when both stream)
+    auto hs = [&](int p0, int p1) {
+      const int64_t n = static_cast<int64_t>(p1 - p0) * (std::max(a.f, a.fs) / g) * (g / 8);
       hsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
         klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), s, e0, e1,
                 a, static_cast<const uint16_t*>(a.h), static_cast<const int32_t*>(nullptr),
-                int64_t{0}, 0, a.Tk, a.f, a.hsum);
+                int64_t{0}, p0, p1, a.f, a.Tk, a.fs, a.hsum);
       });
-    if (S > 0 && p.nt_shared != 0) {
-      const int64_t n2 = static_cast<int64_t>(a.rows - a.Tk) * (a.fs / g) * (g / 8);
-      hsum.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-        klaunch(group_sum_kernel<NM>, dim3(static_cast<unsigned>(cdiv(n2, 256))), dim3(256), s, e0,
-                e1, a, static_cast<const uint16_t*>(a.h), static_cast<const int32_t*>(nullptr),
-                int64_t{0}, a.Tk, a.rows, a.fs, a.hsum);
-      });
-    }
+    };
+    const bool rs = p.nt_routed != 0 && a.Tk > 0, ss = S > 0 && p.nt_shared != 0;
+    if (rs && ss) hs(0, a.rows);
+    else if (rs) hs(0, a.Tk);
+    else if (ss) hs(a.Tk, a.rows);
   }
   add(down, one{}, false, p.nt_routed, p.n_split);
   if (S > 0) add(down, one{}, true, p.nt_shared, p.n_split);
