@@ -136,13 +136,24 @@ def measured_traffic(workload):
     if not os.path.exists(path):
         return None
     kv = dict(re.findall(r"^(\w+): (\S+)$", open(path).read(), flags=re.M))
-    h = hashlib.sha256()
-    for f in ("ffn.hip", "common.hpp"):
-        with open(os.path.join(ROOT, "paper_2503_21135_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    if kv.get("workload") != workload or kv.get("source_sha256_16") != h.hexdigest()[:16]:
+    if kv.get("workload") != workload or kv.get("source_sha256_16") != ffn_source_hash():
         return None
     return int(kv["traffic_bytes_per_launch"])
+
+
+def ffn_source_hash():
+    """Hash of the expert-FFN kernel sources (the counters are valid for them only)."""
+    h = hashlib.sha256()
+    for f in FFN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2503_21135_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+FFN_SOURCES = ("ffn.hip", "ffn_common.hpp", "ffn_prep.hip", "ffn_stream.hip", "ffn_tile.hip",
+               "common.hpp")
+
+
 
 
 def cpu_baseline(wk, inputs, batch, min_seconds):
@@ -487,6 +498,192 @@ def measure_rotated(wk, layer, inputs, hip, n_copies, steps, warmup=5):
             "gate_up_gbs": round(gbs, 1), "gate_up_hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
 
+def pack_copies(wk, n, seed0=0):
+    """n independently packed copies of a workload's layer (seeds seed0..),
+    each with its copy mask of epoch 0 installed."""
+    import moe_inputs as mi
+    import paper_2503_21135_amd as P
+    out = []
+    for r in range(n):
+        inp = mi.LayerInputs(wk.layer, seed=seed0 + r)
+        lay = P.MoELayer(inp, device="cuda:0")
+        lay.set_epoch(0)
+        out.append((lay, inp))
+    return out
+
+
+def roofline_hbm(kernel, nbytes, ms, traffic=None):
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "algorithmic_bytes_per_launch": int(nbytes), "avg_launch_ms": round(ms, 5)}
+
+
+def measure_decode_config(name, copies, hip, steps, warmup):
+    """A decode workload's step (route + FFN + combine) on its layer, once on
+    one packed copy and once rotating over all copies (each with its own
+    batch), so that no copy's weights can still sit in the 256 MB Infinity
+    Cache when its turn comes again.  The gate/up launches are timed by HIP
+    events attached to them; the roofline uses the rotated timing."""
+    import torch
+    import moe_inputs as mi
+    from paper_2503_21135_amd import api
+    wk = mi.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    runs = []
+    for lay, inp in copies:
+        bt = mi.make_batch(wk, inp)
+        xr = torch.from_numpy(bt.x.view(np.int16)).to(dev).view(torch.bfloat16)
+        br = None if bt.bias is None else torch.from_numpy(bt.bias).to(dev)
+        runs.append((lay, xr, br, lay.buffers(wk.tokens)))
+
+    def step(run, evs=None):
+        lay, xr, br, b = run
+        lay.route(xr, br)
+        if evs is None:
+            lay.ffn(xr, b)
+        else:
+            api.moe_expert_ffn_mixed_ev(lay.desc, xr, lay.k, b.offsets, b.perm, b.o, b.ffn_ws, evs)
+        lay.combine(b)
+
+    def timed(order):
+        ev = hip.create(2 * len(order))
+        for i in range(warmup * len(runs)):
+            step(runs[i % len(runs)])
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i, r in enumerate(order):
+            step(runs[r], (C.c_void_p * 5)(None, ev[2 * i], ev[2 * i + 1], None, None))
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / len(order)
+        gu = [hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(len(order))]
+        hip.destroy(ev)
+        return ms, gu
+
+    ms1, gu1 = timed([0] * steps)
+    order = [i % len(runs) for i in range(steps)]
+    msr, gur = timed(order)
+    # each copy routes the same batch every time: its offsets after the runs
+    byt = [algorithmic_bytes(lay, b.offsets.cpu().numpy()) for lay, _, _, b in runs]
+    fl = [algorithmic_flops(lay, b.offsets.cpu().numpy()) for lay, _, _, b in runs]
+    gu_bytes = sum(byt[r]["gate_up"] for r in order) / steps
+    gu_ms = float(np.mean(gur))
+    ffn_bytes = sum(byt[r]["gate_up"] + byt[r]["down"] for r in order) / steps
+    out = {"workload": "%s: %s, T=%d" % (name, wk.layer.name, wk.tokens),
+           "tokens_per_s": round(wk.tokens / (msr * 1e-3), 1), "ms_per_step": round(msr, 5),
+           "steps": steps, "rotated_copies": len(runs),
+           "working_set_mb": round(sum(lay.packed_bytes() for lay, _ in copies) / 1e6, 1),
+           "one_copy": {"ms_per_step": round(ms1, 5),
+                        "tokens_per_s": round(wk.tokens / (ms1 * 1e-3), 1),
+                        "gate_up_ms": round(float(np.mean(gu1)), 5)},
+           "roofline": roofline_hbm("FFN gate/up stage (routed and shared experts)", gu_bytes, gu_ms),
+           "step_weight_bytes": int(ffn_bytes),
+           "step_hbm_frac": round(ffn_bytes / (msr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "step_tflops": round(sum(fl[r] for r in order) / steps / (msr * 1e-3) / 1e12, 2),
+           "expert_rows_copy0": [int(v) for v in np.diff(runs[0][3].offsets.cpu().numpy())]}
+    runs.clear()
+    return out
+
+
+def measure_stress(hip, n_copies, steps=None):
+    """The runtime-switch stress workload on the Qwen1.5-MoE-A2.7B-shaped
+    layer: 512 fresh tokens per step, the copy mask redrawn every 10 steps,
+    the steps rotating over n_copies independently packed copies of the
+    layer (each mask update installs the new epoch on every copy).  Steady
+    throughput is the median step (device events around route + FFN +
+    combine); switch latency is the host wall time of installing one copy's
+    three slot lists until the stream is idle, and its device time."""
+    import torch
+    import moe_inputs as mi
+    from paper_2503_21135_amd import api
+    wk = mi.WORKLOADS["qwen-stress"]
+    steps = wk.steps if steps is None else steps
+    copies = pack_copies(wk, n_copies)
+    n_ep = (steps + wk.redraw_every - 1) // wk.redraw_every
+    xs = []
+    for st in range(min(steps, 20)):   # distinct batches, reused cyclically
+        bt = mi.make_batch(wk, copies[0][1], step=st)
+        xs.append(torch.from_numpy(bt.x.view(np.int16)).to("cuda:0").view(torch.bfloat16))
+    bufs = [lay.buffers(wk.tokens) for lay, _ in copies]
+    sptr = torch.cuda.current_stream().cuda_stream
+    ev = hip.create(4 * steps)
+    ev_sw = hip.create(2 * n_ep * n_copies)
+    host_sw = []
+    torch.cuda.synchronize()
+    for st in range(steps):
+        if st % wk.redraw_every == 0:
+            ep = st // wk.redraw_every
+            for c, (lay, inp) in enumerate(copies):
+                slots = [np.ascontiguousarray(inp.slots_on(kd, ep), np.int32) for kd in range(3)]
+                torch.cuda.synchronize()
+                w0 = time.perf_counter()
+                i = 2 * (ep * n_copies + c)
+                hip.record(ev_sw[i], sptr)
+                for kd in range(3):
+                    api.moe_set_channel_switch(lay.desc, kd, slots[kd])
+                hip.record(ev_sw[i + 1], sptr)
+                torch.cuda.synchronize()
+                host_sw.append(time.perf_counter() - w0)
+        lay, _ = copies[st % n_copies]
+        b = bufs[st % n_copies]
+        x = xs[st % len(xs)]
+        hip.record(ev[4 * st], sptr)
+        lay.route(x)
+        api.moe_expert_ffn_mixed_ev(lay.desc, x, lay.k, b.offsets, b.perm, b.o, b.ffn_ws,
+                                    (C.c_void_p * 5)(ev[4 * st + 1], None, None, None,
+                                                     ev[4 * st + 2]))
+        lay.combine(b)
+        hip.record(ev[4 * st + 3], sptr)
+    torch.cuda.synchronize()
+    step_ms = np.array([hip.ms(ev[4 * i], ev[4 * i + 3]) for i in range(steps)])
+    ffn_ms = np.array([hip.ms(ev[4 * i + 1], ev[4 * i + 2]) for i in range(steps)])
+    sw_dev = np.array([hip.ms(ev_sw[2 * i], ev_sw[2 * i + 1]) for i in range(n_ep * n_copies)])
+    hip.destroy(ev)
+    hip.destroy(ev_sw)
+    # bytes and flops of the last step of each copy (its routing and mask)
+    byt, fl = [], []
+    for (lay, _), b in zip(copies, bufs):
+        off = b.offsets.cpu().numpy()
+        bb = algorithmic_bytes(lay, off)
+        byt.append(bb["gate_up"] + bb["down"])
+        fl.append(algorithmic_flops(lay, off))
+    med, ffn_med = float(np.median(step_ms)), float(np.median(ffn_ms))
+    nb, nf = float(np.mean(byt)), float(np.mean(fl))
+    ws_mb = round(sum(lay.packed_bytes() for lay, _ in copies) / 1e6, 1)
+    pcts = [int(copies[0][1].switch_percent(e)) for e in range(n_ep)]
+    copies.clear()
+    bufs.clear()
+    torch.cuda.empty_cache()
+    gbs = nb / (ffn_med * 1e-3) / 1e9
+    tf = nf / (ffn_med * 1e-3) / 1e12
+    return {"workload": "%s: T=%d x %d steps, mask redrawn every %d steps (%d epochs, %d-%d%% of "
+                        "rows switched), rotating over %d packed copies"
+                        % (wk.name, wk.tokens, steps, wk.redraw_every, n_ep, min(pcts), max(pcts),
+                           n_copies),
+            "steady_tokens_per_s": round(wk.tokens / (med * 1e-3), 1),
+            "step_ms_median": round(med, 4),
+            "step_ms_p10": round(float(np.percentile(step_ms, 10)), 4),
+            "step_ms_p90": round(float(np.percentile(step_ms, 90)), 4),
+            "ffn_ms_median": round(ffn_med, 4),
+            "working_set_mb": ws_mb,
+            "switch_host_ms_median": round(float(np.median(host_sw)) * 1e3, 4),
+            "switch_device_ms_median": round(float(np.median(sw_dev)), 4),
+            "switched_percent_by_epoch": pcts,
+            "roofline": {"bound": "hbm", "kernel": "expert FFN (both stages) per step; near the "
+                                                  "ridge, so both fractions are given",
+                         "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "mfma_achieved_tflops": round(tf, 1),
+                         "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                         "algorithmic_bytes_per_step": int(nb),
+                         "algorithmic_flops_per_step": int(nf)},
+            "verified": "every step's routing (all 512 tokens, bit-exact) and output (8 tokens) "
+                        "against the oracle in tests/test_gpu_stress.py"}
+
+
 def measure_copy(mib=1024, reps=10):
     """GB/s of a plain device-to-device copy (bytes read + written), for context."""
     import torch
@@ -589,6 +786,11 @@ def main():
                     help="skip the timing of a requantization for a new dataset")
     ap.add_argument("--no-bf16", action="store_true",
                     help="skip the unquantized bf16 reference of the same step")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (DeepSeekMoE-shaped decode and prefill, "
+                         "Qwen-shaped switch stress) that the default run also measures")
+    ap.add_argument("--config-rotate", type=int, default=3, metavar="N",
+                    help="packed copies the other workloads rotate over (Infinity Cache defeat)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device-to-device copies of MIB MiB (the "
                          "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -732,6 +934,23 @@ def main():
         # last: it rewrites the layer's copies
         extra["dataset_switch"] = measure_dataset_switch(layer, inputs, hip, ms_per_step)
         log("dataset switch", extra["dataset_switch"])
+
+    if args.workload == "mixtral-decode" and not args.no_configs:
+        # the other workloads, each on its own layer
+        import moe_inputs as mi
+        n = max(1, args.config_rotate)
+        log("deepseek-decode / -prefill: packing %d copies" % n)
+        ds = pack_copies(mi.WORKLOADS["deepseek-decode"], n)
+        extra["deepseek_decode"] = measure_decode_config("deepseek-decode", ds, hip, min(K, 100), 5)
+        log("deepseek decode", extra["deepseek_decode"])
+        extra["deepseek_prefill"] = measure_prefill(ds[0][0], ds[0][1], "deepseek-prefill", hip,
+                                                    args.prefill_steps, 5, bf16=False)
+        log("deepseek prefill", extra["deepseek_prefill"])
+        ds.clear()
+        torch.cuda.empty_cache()
+        log("qwen-stress: %d copies, %d steps" % (n, mi.WORKLOADS["qwen-stress"].steps))
+        extra["qwen_stress"] = measure_stress(hip, n)
+        log("qwen stress", extra["qwen_stress"])
 
     cpu = None
     if not args.no_cpu_baseline:

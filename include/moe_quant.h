@@ -24,7 +24,12 @@
  * ---------------------------------------
  *   - Every buffer is owned by the caller.  "device" pointers are HIP device
  *     memory, "host" pointers are ordinary host memory read only during the
- *     call.  The library keeps no state between calls and allocates nothing.
+ *     call.  The library allocates no device memory and keeps no state about
+ *     any layer or batch between calls.  It caches three host-side facts:
+ *     the compute-unit count of each device (read once per device, used to
+ *     size the prefill grid), the MOE_DEBUG setting (read once), and
+ *     per-thread scratch vectors that moe_set_channel_switch reuses for its
+ *     host validation.
  *   - All device work is enqueued on `stream` (a hipStream_t, passed as void*;
  *     NULL is the default stream) and is asynchronous to the host.  No entry
  *     point reads device memory back to the host.
@@ -75,9 +80,12 @@
  *     and zero point are applied to the fp32 partial sum;
  *   - more tokens (prefill): as the 16-bit dequantized
  *     operand of the paper (Sec. V-B), fp16(s * (q - z)) -- one rounding per
- *     weight -- multiplied by fp16 copies of the activations and of h.  The
- *     bf16 values convert to fp16 exactly while |value| < 65504; larger
- *     activations or hidden values are outside this path's domain.
+ *     weight -- multiplied by fp16 copies of the activations and of h.  A
+ *     bf16 value converts to fp16 exactly when it is 0 or its magnitude lies
+ *     in [2^-17, 65504]; below 2^-17 it is rounded to the fp16 subnormal grid
+ *     (absolute error <= 2^-25); beyond 65504 (and for inf or NaN) it has no
+ *     finite fp16 value, and the call reports it through its status word
+ *     (MOE_ERR_RANGE) instead of silently producing infinities.
  * Either way the FFN output matches the exact definition to within 2e-3
  * relative L2 (measured: ~1e-4 for the first, ~1.1e-3 for the second).
  */
@@ -99,8 +107,9 @@ extern "C" {
 #define MOE_ERR_WORKSPACE -4  /* workspace NULL or smaller than the size helper returns */
 #define MOE_ERR_SLOT      -5  /* switch slot out of range, duplicated, or two slots
                                  naming the same (expert, row)                          */
-#define MOE_ERR_RANGE     -6  /* an fp16 scale would overflow (reported by the device
-                                 status word of moe_quant_pack)                         */
+#define MOE_ERR_RANGE     -6  /* a value outside fp16's range: a scale in moe_quant_pack
+                                 or moe_requant_channels, an activation or hidden value
+                                 of the FFN's fp16 operand path (device status words) */
 #define MOE_ERR_HIP       -7  /* a HIP call or kernel launch failed                    */
 
 /* Limits checked by the host validation. */
@@ -291,14 +300,20 @@ int moe_ffn_plan(const moe_layer_t* L, int32_t T, int32_t k,
  *   o          device fp32 [n_split][T*(k+S)][d_model]; the FFN output of row p
  *              is the sum over the n_split slices (moe_ffn_plan), which
  *              moe_unpermute_combine adds.  16-byte aligned.
- *   ws         device workspace of at least moe_ffn_plan()'s ws_bytes.
+ *   ws         device workspace of at least moe_ffn_plan()'s ws_bytes; scratch
+ *              between calls (no initialization needed).
+ *   status     device int32 or NULL; set to MOE_ERR_RANGE when the fp16 operand
+ *              path (prefill sizes, see "FFN numerics") meets an activation or
+ *              a hidden value with no finite fp16 value (|v| > 65504, inf,
+ *              NaN); the outputs of that call are then not valid.  Never
+ *              cleared by the library; the streaming (decode) path never sets it.
  *   Never reads offsets on the host: the grid covers the worst case and idle
  *   waves exit.
  */
 int moe_expert_ffn_mixed(const moe_layer_t* L, const uint16_t* x, int32_t T,
                          int32_t k, const int32_t* offsets,
                          const int32_t* perm_token, float* o,
-                         void* ws, size_t ws_bytes, void* stream);
+                         void* ws, size_t ws_bytes, int32_t* status, void* stream);
 
 /*
  * moe_expert_ffn_mixed_ev -- moe_expert_ffn_mixed that also records HIP
@@ -319,7 +334,7 @@ int moe_expert_ffn_mixed(const moe_layer_t* L, const uint16_t* x, int32_t T,
 int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
                             int32_t k, const int32_t* offsets,
                             const int32_t* perm_token, float* o,
-                            void* ws, size_t ws_bytes, void* stream,
+                            void* ws, size_t ws_bytes, int32_t* status, void* stream,
                             void* const* events, int32_t n_events);
 
 /*
@@ -373,10 +388,16 @@ int moe_requant_channels(moe_layer_t* L, int32_t kind, const uint16_t* cache,
                          int32_t* status, void* stream);
 
 /*
- * moe_unpermute_combine -- y[t] = sum_j topk_w[t][j] * o[inv_perm[t][j]]
- *                                + sum_s o[inv_perm[t][k+s]],
- * where o[p] = sum over the n_split slices at o + i*split_stride.  fp32.
- *   y device fp32 [T][d]; o, y 16-byte aligned, d % 4 == 0.
+ * moe_unpermute_combine -- the MoE output of each token, Sec. II-A: the
+ * outputs of the k selected experts weighted by the router's combine weights
+ * (plus the shared experts with weight 1), back in token order:
+ *   y[t] = sum_j topk_w[t][j] * o[inv_perm[t][j]] + sum_s o[inv_perm[t][k+s]],
+ * where o[p] = sum over the n_split slices at o + i*split_stride (slice 0
+ * first).  fp32, fused multiply-adds in the order written (slot 0 first), so
+ * the result is bitwise reproducible.
+ *   o         device fp32 [n_split] slices of [T*(k+S)][d] (moe_expert_ffn_mixed)
+ *   inv_perm, topk_w   from moe_route_permute
+ *   y         device fp32 [T][d]; o, y 16-byte aligned, d % 4 == 0.
  */
 int moe_unpermute_combine(const float* o, int32_t n_split, int64_t split_stride,
                           const int32_t* inv_perm, const float* topk_w,

@@ -312,11 +312,60 @@ def effective_weight(w_fp32: np.ndarray, bits: int, group: int,
     return W
 
 
+class LayerWeights:
+    """The dequantized weights of a layer, built once, for checking many
+    batches and switch masks (the 8-bit-copy mode of ``effective_weight``).
+
+    Per (expert, kind): the dequantized base codes at the expert's precision
+    (Sec. IV-A) and the dequantized 8-bit copies of every row a copy header
+    names (Sec. IV-B, V-A).  ``effective(e, kind, switched)`` returns the
+    matrix the FFN sees when `switched` rows read their copies.  The copy of
+    a row is the quantization of that row alone, so quantizing every cached
+    row at once gives each row the codes ``effective_weight`` gives it.
+    """
+
+    def __init__(self, layer, experts=None):
+        cfg = layer.cfg
+        self.group = cfg.group
+        self.base = {}
+        self.copy_rows = {}
+        self.copy = {}
+        hdr = {kind: np.asarray(layer.copy_headers(kind), np.int64).reshape(-1, 2) for kind in (0, 1, 2)}
+        for e in (range(cfg.n_experts + cfg.n_shared) if experts is None else experts):
+            for kind in (0, 1, 2):
+                w = layer.weight(e, kind)
+                st, q, s, z = quantize(w, int(layer.bits[e]), cfg.group)
+                if st != OK:
+                    raise ValueError("oracle quantize: status %d" % st)
+                self.base[(e, kind)] = dequant(q, s, z, cfg.group)
+                rows = np.unique(hdr[kind][hdr[kind][:, 0] == e, 1]) if e < cfg.n_experts else \
+                    np.zeros(0, np.int64)
+                self.copy_rows[(e, kind)] = rows
+                if len(rows):
+                    st, q8, s8, z8 = quantize(w[rows], 8, cfg.group)
+                    if st != OK:
+                        raise ValueError("oracle quantize: status %d" % st)
+                    self.copy[(e, kind)] = dequant(q8, s8, z8, cfg.group)
+
+    def effective(self, e: int, kind: int, switched: Optional[np.ndarray]) -> np.ndarray:
+        W = self.base[(e, kind)]
+        if switched is None or len(switched) == 0:
+            return W
+        rows = self.copy_rows[(e, kind)]
+        idx = np.searchsorted(rows, switched)
+        if np.any(idx >= len(rows)) or np.any(rows[np.minimum(idx, len(rows) - 1)] != switched):
+            raise ValueError("a switched row of expert %d, kind %d has no cached copy" % (e, kind))
+        W = W.copy()
+        W[switched] = self.copy[(e, kind)][idx]
+        return W
+
+
 def layer_forward(layer, x_bits: np.ndarray, bias: Optional[np.ndarray] = None,
                   row_slot: Optional[Dict[int, np.ndarray]] = None,
                   round_h: bool = True, tokens: Optional[np.ndarray] = None,
                   weight_cache: Optional[dict] = None,
-                  copy_bits: Optional[Dict[int, np.ndarray]] = None):
+                  copy_bits: Optional[Dict[int, np.ndarray]] = None,
+                  weights: Optional[LayerWeights] = None):
     """One MoE layer on the CPU.
 
     layer     moe_inputs.LayerInputs (weights are drawn from it)
@@ -326,8 +375,11 @@ def layer_forward(layer, x_bits: np.ndarray, bias: Optional[np.ndarray] = None,
               the cached 16-bit channels (layer.channel_cache), or None
     tokens    optional subset of token indices whose outputs are computed
               (routing is always done for all tokens)
-    Returns dict with logits, topk_ids, topk_w, offsets, perm, inv and y
-    (y rows for `tokens`, float64).
+    weights   optional LayerWeights of the same layer (8-bit-copy mode only):
+              its dequantized matrices are used instead of quantizing afresh
+    Returns dict with logits, topk_ids, topk_w, offsets, perm, inv, y (y rows
+    for `tokens`, float64), o_rows (the permuted rows whose expert output was
+    computed, ascending) and o (those rows' expert outputs, float64).
     """
     cfg = layer.cfg
     E, S, k = cfg.n_experts, cfg.n_shared, cfg.top_k
@@ -356,12 +408,16 @@ def layer_forward(layer, x_bits: np.ndarray, bias: Optional[np.ndarray] = None,
                     cb = int(copy_bits[kind][e])
                 if cb and len(sw):
                     src = layer.channel_cache(kind)[row_slot[kind][e][sw]]
-            W = effective_weight(layer.weight(e, kind), int(layer.bits[e]), cfg.group, sw,
-                                 cb, src)
+            if weights is not None and cb == 0:
+                W = weights.effective(e, kind, sw)
+            else:
+                W = effective_weight(layer.weight(e, kind), int(layer.bits[e]), cfg.group, sw,
+                                     cb, src)
             if weight_cache is not None:
                 weight_cache[key] = W
             Ws.append(W)
         o[rows_p] = expert_ffn(Ws[0], Ws[1], Ws[2], x_bits, perm[rows_p], round_h)
     y = combine(o, inv[sel], w[sel], k, S)
+    o_rows = np.nonzero(need)[0]
     return dict(logits=logits, topk_ids=ids, topk_w=w, offsets=offsets,
-                perm=perm, inv=inv, y=y, tokens=sel)
+                perm=perm, inv=inv, y=y, tokens=sel, o_rows=o_rows, o=o[o_rows])

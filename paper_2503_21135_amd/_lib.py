@@ -71,9 +71,9 @@ def load() -> C.CDLL:
         "moe_code_row_words": (i64, [i32, i32]),
         "moe_ffn_plan": (C.c_int, [C.POINTER(LayerDesc), i32, i32, C.POINTER(i32), C.POINTER(sz_t)]),
         "moe_expert_ffn_mixed": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
-                                           sz_t, vp]),
+                                           sz_t, vp, vp]),
         "moe_expert_ffn_mixed_ev": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
-                                              sz_t, vp, vp, i32]),
+                                              sz_t, vp, vp, vp, i32]),
         "moe_set_channel_switch": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i32, vp]),
         "moe_requant_channels": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i64, vp, vp, vp]),
         "moe_unpermute_combine": (C.c_int, [vp, i32, i64, vp, vp, i32, i32, i32, i32, vp, vp]),

@@ -86,25 +86,28 @@ def moe_ffn_plan(desc: LayerDesc, T: int, k: int) -> Tuple[int, int]:
 
 def moe_expert_ffn_mixed(desc: LayerDesc, x: torch.Tensor, k: int, offsets: torch.Tensor,
                          perm_token: torch.Tensor, o: torch.Tensor, ws: torch.Tensor,
-                         stream=None) -> None:
-    """Grouped mixed-precision SiLU-GLU expert FFN (Sec. IV-A, IV-B, V-B)."""
-    _need_cuda(x, offsets, perm_token, o, ws)
+                         status: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Grouped mixed-precision SiLU-GLU expert FFN (Sec. IV-A, IV-B, V-B).
+    `status` (device int32, optional) receives MOE_ERR_RANGE when the fp16
+    operand path meets a value beyond fp16's range."""
+    _need_cuda(x, offsets, perm_token, o, ws, status)
     T = x.shape[0]
     st = load().moe_expert_ffn_mixed(C.byref(desc), _p(x), T, k, _p(offsets), _p(perm_token),
-                                     _p(o), _p(ws), ws.numel() * ws.element_size(), _s(stream))
+                                     _p(o), _p(ws), ws.numel() * ws.element_size(), _p(status),
+                                     _s(stream))
     check(st, "moe_expert_ffn_mixed")
 
 
 def moe_expert_ffn_mixed_ev(desc: LayerDesc, x: torch.Tensor, k: int, offsets: torch.Tensor,
                             perm_token: torch.Tensor, o: torch.Tensor, ws: torch.Tensor,
-                            events, stream=None) -> None:
+                            events, status: Optional[torch.Tensor] = None, stream=None) -> None:
     """moe_expert_ffn_mixed recording caller-created hipEvent_t handles
     (a ctypes c_void_p array) at its stage boundaries."""
-    _need_cuda(x, offsets, perm_token, o, ws)
+    _need_cuda(x, offsets, perm_token, o, ws, status)
     T = x.shape[0]
     st = load().moe_expert_ffn_mixed_ev(C.byref(desc), _p(x), T, k, _p(offsets), _p(perm_token),
-                                        _p(o), _p(ws), ws.numel() * ws.element_size(), _s(stream),
-                                        C.cast(events, C.c_void_p), len(events))
+                                        _p(o), _p(ws), ws.numel() * ws.element_size(), _p(status),
+                                        _s(stream), C.cast(events, C.c_void_p), len(events))
     check(st, "moe_expert_ffn_mixed_ev")
 
 

@@ -71,6 +71,10 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return u >> 16;
 }
 
+// true when f converts to a finite binary16 value (|f| <= 65504; NaN and
+// larger magnitudes do not)
+__device__ __forceinline__ bool fp16_finite(float f) { return __builtin_fabsf(f) <= 65504.0f; }
+
 __device__ __forceinline__ float fp16_bits_to_f32(uint32_t h) {
   return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
 }

@@ -1,0 +1,502 @@
+// ffn_tile.hip -- the tile kernel of moe_expert_ffn_mixed, for experts with
+// many tokens (prefill sizes), and its work-plan kernel.
+#include "ffn_common.hpp"
+
+namespace moe {
+namespace ffn {
+
+// ------------------------------------------------------------------ tile kernel
+// For experts with many tokens (prefill, shared experts), where the
+// contraction is MFMA-bound: a workgroup computes a tile of kTileTok tokens x
+// kTileRowsOf<NK> row positions with v_mfma_f32_32x32x16_f16.  This is
+// the paper's formulation of the dequantized product (Sec. V-B: dequantize to
+// a 16-bit operand, then matrix-core multiply): the weight operand is
+// fp16(s * (q - z)) -- one rounding per weight -- and the activations enter
+// as fp16 (the bf16 activations and hidden values convert exactly while
+// their magnitude stays below 65504).  The scale is thus inside the operand
+// and the accumulation runs over the whole K with no per-group epilogue.
+//
+// Dequantization: a code q OR-ed into the mantissa of fp16 1024.0 gives
+// exactly 1024 + q (q < 1024); one packed fp16 subtraction of 1024 + z makes
+// q - z exactly, one packed fp16 multiplication by s rounds the product.
+//
+// Eight waves per workgroup, two per SIMD.  Each wave owns 32 rows of one
+// kind (gate/up: waves 0-3 the gate rows, 4-7 the up rows of the tile's 128
+// positions; down: 256 rows) and all kTileTok tokens (four 32-token blocks),
+// so every dequantized B fragment feeds four MFMAs.  Lane l holds row l % 32
+// and the K-half l/32 of each group (group code g/2*half + 8*s + j feeds
+// K-step s, slot j); accumulator element r of lane l is token
+// 8*(r/4) + 4*(l/32) + r%4 of the block.  The activations of one group for
+// the whole tile are staged in LDS by direct-to-LDS loads, two groups ahead
+// (three stages), with the XOR swizzle of the streaming kernel; the packed
+// codes of the next three groups are in flight in registers.  The SiLU-GLU
+// epilogue meets the gate and up sums of a row through LDS.
+//
+// Work items (expert, row block, token tile) come from a prefix table a small
+// plan kernel builds from the routing offsets and class counts, and are
+// spread over a persistent grid so that the workgroups of one XCD (hardware
+// places workgroup b on XCD b % 8) take consecutive items.  Within an expert
+// the items run in super-tiles of kSuper row blocks x kSuper token tiles, so
+// that the workgroups one XCD runs together share both their code rows and
+// their activation rows through that XCD's L2.
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                 0, 0);
+}
+
+constexpr uint32_t kMagic16 = 0x64006400u;   // two fp16 1024.0
+
+// LDS of the tile kernel: three stages of kTileTok token rows x g columns of
+// fp16 activations in 16-byte slots (slot s: token s / (g/8), column chunk
+// (s % (g/8)) ^ (token % (g/8))).
+template <int NM2>
+struct HTile {
+  static constexpr int g = NM2 * 16;
+  static constexpr int SPT = g / 8;
+  static constexpr int SLOTS = kTileTok * SPT;
+  union {
+    u32x4 a[3][SLOTS];
+    float xch[4 * 4 * 16 * 64];   // gate/up epilogue: the up sums of four 32-row blocks
+  };
+};
+
+
+// Items of expert e: (row blocks over its classes) x (token tiles); the
+// exclusive prefix over the launch's experts goes to prefix[0 .. n_e].
+template <int NK>
+__global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, int32_t* __restrict__ prefix) {
+  __shared__ int cnt[MOE_MAX_EXPERTS];
+  const int i = threadIdx.x;
+  int items = 0;
+  if (i < map.n_e) {
+    const int e = map.e0 + i;
+    const int n_tok = a.offsets[e + 1] - a.offsets[e];
+    const int tiles = (n_tok + kTileTok - 1) / kTileTok;
+    int blocks = 0;
+    if (e < a.E) {
+      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) blocks += (cc[c] + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
+    } else {
+      blocks = ((NK == 1 ? a.d : a.fs) + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
+    }
+    items = tiles * blocks;
+  }
+  if (i < MOE_MAX_EXPERTS) cnt[i] = items;
+  __syncthreads();
+  if (i == 0) {
+    int acc = 0;
+    for (int j = 0; j < map.n_e; j++) {
+      const int v = cnt[j];
+      prefix[j] = acc;
+      acc += v;
+    }
+    prefix[map.n_e] = acc;
+  }
+}
+
+// One lane's source of one kind: resources, {s, z} group stride and offsets.
+struct TSrc {
+  Rsrc code, sz;
+  uint32_t sz_gstride, coff, soff;
+};
+
+// Packed-code words of one lane's half of a group (g/2 codes).
+template <int NM2, int B>
+constexpr int kHalfWords = NM2 * 16 / 2 * B / 32;
+
+// fp16 pair (1024 + q_lo, 1024 + q_hi) from two codes at bit offset sh of
+// each half-word (b <= 8 bits wide, masked by m).
+__device__ __forceinline__ uint32_t unpack16(uint32_t w, int sh, uint32_t m, uint32_t vm) {
+  return ((w >> sh) & m) | vm;
+}
+
+// B fragment of K-step s: 8 fp16 weights s*(q - z) of this lane's row.
+template <int NM2, int B>
+__device__ __forceinline__ u32x4 dequant_h(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, f16x2 zneg, f16x2 sc,
+                                           uint32_t vm) {
+  uint32_t r[4];
+  if constexpr (B == 4) {
+    const uint32_t w = cw[s];
+#pragma unroll
+    for (int i = 0; i < 4; i++) r[i] = unpack16(w, 4 * i, 0x000F000Fu, vm);
+  } else if constexpr (B == 8) {
+    const uint32_t w0 = cw[2 * s], w1 = cw[2 * s + 1];   // bytes (c0, c2, c1, c3)
+    r[0] = unpack16(w0, 0, 0x00FF00FFu, vm);
+    r[1] = unpack16(w0, 8, 0x00FF00FFu, vm);
+    r[2] = unpack16(w1, 0, 0x00FF00FFu, vm);
+    r[3] = unpack16(w1, 8, 0x00FF00FFu, vm);
+  } else if constexpr (B == 2) {
+    const uint32_t w = cw[s >> 1];
+    const int o = (s & 1) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; i++) r[i] = unpack16(w, o + 2 * i, 0x00030003u, vm);
+  } else if constexpr (B == 6) {  // per 32-code block: words 0-3 bits 0..3, words 4-5 bits 4..5
+    const int blk = 6 * (s >> 2);
+    const int q = s & 3;   // octet within the block
+    const uint32_t lo = cw[blk + q], hi = cw[blk + 4 + (q >> 1)];
+    const int o = (q & 1) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+      r[i] = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | vm;
+  } else {  // 3-bit: per 32-code block words (low plane 0-15, low plane 16-31, high plane)
+    const int blk = 3 * (s >> 2);
+    const int q = s & 3;   // octet within the block
+    const uint32_t lo = cw[blk + (q >> 1)], hi = cw[blk + 2];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int pi = 4 * q + i;   // pair index within the block
+      r[i] = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | vm;
+    }
+  }
+  u32x4 out;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const f16x2 d = __builtin_bit_cast(f16x2, r[i]) + zneg;   // q - z, exact
+    out[i] = __builtin_bit_cast(uint32_t, d * sc);            // s * (q - z), rounded once
+  }
+  return out;
+}
+
+// {s, z} word -> packed (-(1024 + z), -(1024 + z)) and (s, s).
+__device__ __forceinline__ void sz_pair(uint32_t w, f16x2& zneg, f16x2& sc) {
+  const _Float16 s16 = __builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xFFFFu));
+  const _Float16 z16 = __builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16));
+  const _Float16 zn = -(z16 + static_cast<_Float16>(1024.0f));   // exact: integer <= 1279
+  zneg = f16x2{zn, zn};
+  sc = f16x2{s16, s16};
+}
+
+template <int NM2, int BW>
+struct HCodes {
+  uint32_t cw[(kHalfWords<NM2, BW>)];
+  uint32_t szw;
+};
+
+template <int NM2, int BW>
+__device__ __forceinline__ void hload(HCodes<NM2, BW>& st, const TSrc& sr, int gi, bool gv) {
+  constexpr uint32_t gcb = NM2 * 16 * BW / 8;   // code bytes per row and group
+  bload<kHalfWords<NM2, BW>>(st.cw, sr.code, gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
+  st.szw = __builtin_amdgcn_raw_buffer_load_b32(sr.sz, gv ? sr.soff : kOOB, gv ? gi * sr.sz_gstride : 0u, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void hwait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Barrier without __syncthreads()' fences (those would drain the in-flight
+// code loads); the LDS stages are ordered by the explicit waits around it.
+__device__ __forceinline__ void tile_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// silu(g) * u with a hardware reciprocal: h is rounded to bf16 right after,
+// far coarser than the reciprocal's error.
+__device__ __forceinline__ float silu_mul_fast(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
+
+// Activation stages in flight: the stage of group gi+2 is loaded while group
+// gi is contracted; three LDS stages.
+constexpr int kAStages = 3;
+
+// One wave's share of a tile item: 32 rows (position block rb) of weight kind
+// kk, whose source has width BW (the expert's base width, or 8 for the
+// cached copies of a switched class), against all kTileTok tokens.
+template <int NM2, int NK, int BW, int TB>
+__device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int e, bool copy, int be, int kk,
+                                          int rb, int pos0, int pos1, int R, int t0, int t1) {
+  constexpr int g = NM2 * 16;
+  constexpr int SPT = HTile<NM2>::SPT;
+  // activation slots of the tile's TB token blocks, and loads per thread and
+  // stage (slots past them are written with zeros)
+  constexpr int SL = TB * 32 * SPT;
+  constexpr int NLD = (SL + 64 * kTileWaves - 1) / (64 * kTileWaves);
+  constexpr bool down = NK == 1;
+  // vector-memory instructions of one group's code and {s, z} loads
+  constexpr int LC = kCodeLoads<(kHalfWords<NM2, BW>)> + 1;
+  const int tid = threadIdx.x;
+  const int wv = tid >> 6, lane = tid & 63;
+  const int n = lane & 31, kh = lane >> 5;
+  const bool routed = e < a.E;
+  const int K = down ? (routed ? a.f : a.fs) : a.d;
+  const int G = K / g;
+  const int kind0 = down ? 2 : 0;
+  const int32_t* order = down ? a.order_dn : a.order_gu;
+  const int pos = pos0 + 32 * rb + n;
+  const bool live = pos < pos1;
+  const int row = live ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+
+  TSrc src;
+  {
+    const KindDev& kd = a.kd[kind0 + kk];
+    const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
+    const uint32_t crow_bytes = 4u * static_cast<uint32_t>(code_row_words(K, 8));
+    const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
+                            : static_cast<const void*>(kd.codes + uni(kd.code_off[e]));
+    const void* sptr = copy ? static_cast<const void*>(kd.copy_sz)
+                            : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
+    const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
+    const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
+    src.code = make_rsrc(cptr, cbytes);
+    src.sz = make_rsrc(sptr, sbytes);
+    src.sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
+    const int slot = (copy && live) ? kd.row_slot[static_cast<int64_t>(e) * R + row] : -1;
+    const uint32_t c_base = live ? row * row_bytes + kh * (g / 2) * be / 8 : kOOB;
+    const uint32_t s_base = live ? row * 4u : kOOB;
+    const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * crow_bytes + kh * (g / 2) : kOOB;
+    const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
+    src.coff = copy ? c_copy : c_base;
+    src.soff = copy ? s_copy : s_base;
+  }
+  // fp16 activations: gathered x rows (gate/up) or h rows (down), row p of the
+  // permuted order; slot i of this thread's loads
+  const Rsrc xr = make_rsrc(down ? static_cast<const void*>(a.h) : static_cast<const void*>(a.x16),
+                            down ? a.h_bytes : a.x16_bytes);
+  uint32_t aoff[NLD];
+#pragma unroll
+  for (int i = 0; i < NLD; i++) {
+    const int sl = tid + 64 * kTileWaves * i;
+    const int t = sl / SPT;
+    const int c = (sl % SPT) ^ (t % SPT);
+    const int p = t0 + t;
+    aoff[i] = (sl < SL && p < t1)
+                  ? static_cast<uint32_t>(2 * (down ? h_row(a, p) : static_cast<int64_t>(a.perm[p]) * K) + 16 * c)
+                  : kOOB;
+  }
+  auto stage_a = [&](int buf, int gi) {
+    const bool gv = gi < G;
+    const uint32_t adv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
+#pragma unroll
+    for (int i = 0; i < NLD; i++)
+      lds_dma16(xr, &tl.a[buf][64 * kTileWaves * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
+  };
+
+  // the OR operand of the unpacking in a vector register (one v_and_or_b32)
+  uint32_t vm = kMagic16;
+  asm volatile("" : "+v"(vm));
+  f32x16 acc[TB];
+#pragma unroll
+  for (int tb = 0; tb < TB; tb++) acc[tb] = f32x16{};
+
+  HCodes<NM2, BW> cs[3];
+  stage_a(0, 0);
+  hload<NM2, BW>(cs[0], src, 0, 0 < G);
+  stage_a(1, 1);
+  hload<NM2, BW>(cs[1], src, 1, 1 < G);
+  hload<NM2, BW>(cs[2], src, 2, 2 < G);
+  hwait_vm<2 * LC + NLD>();   // activations of group 0 have landed (this wave's share)
+  tile_barrier();             // ... every wave's share
+
+  auto group = [&](HCodes<NM2, BW>& c, int buf, int gi) {
+    stage_a((buf + 2) % kAStages, gi + 2);   // that stage was last read for group gi-1 (barrier since)
+    if (gi < G) {   // workgroup-uniform (G is odd for some shapes)
+      f16x2 zn, sc;
+      sz_pair(c.szw, zn, sc);
+#pragma unroll
+      for (int s = 0; s < NM2; s++) {
+        u32x4 af[TB];
+#pragma unroll
+        for (int tb = 0; tb < TB; tb++) {
+          const int t = tb * 32 + n;
+          af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
+        }
+        const u32x4 bf = dequant_h<NM2, BW>(c.cw, s, zn, sc, vm);
+#pragma unroll
+        for (int tb = 0; tb < TB; tb++) acc[tb] = mfma32h(af[tb], bf, acc[tb]);
+      }
+    }
+    hload<NM2, BW>(c, src, gi + 3, gi + 3 < G);
+    hwait_vm<2 * LC + NLD>();   // everything but the last two code loads and the newest stage: group gi+1's
+    tile_barrier();
+  };
+  for (int gi = 0; gi < G; gi += 3) {
+    group(cs[0], 0, gi);
+    group(cs[1], 1, gi + 1);
+    group(cs[2], 2, gi + 2);
+  }
+  hwait_vm<0>();
+
+  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4, row `row`
+  if constexpr (NK == 2) {
+    // the up waves hand their sums to the gate waves of the same rows through
+    // the (now idle) activation stages; same lane layout on both sides
+    float* xch = tl.xch;
+    tile_barrier();   // every wave is done reading the activation stages
+    if (kk == 1) {
+#pragma unroll
+      for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) xch[((rb * 4 + tb) * 16 + r) * 64 + lane] = acc[tb][r];
+    }
+    tile_barrier();
+    if (kk == 0) {
+      // rows of one item are all routed or all shared: one h row width
+      const int hw = t0 < a.Tk ? a.f : a.fs;
+      uint16_t* hbase = a.h + h_row(a, t0 + 4 * kh) + row;
+      bool bad = false;
+#pragma unroll
+      for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+          const float u = xch[((rb * 4 + tb) * 16 + r) * 64 + lane];
+          if (live && t0 + 4 * kh + dt < t1) {
+            // h = bf16(silu(g) * u), stored as its fp16 value (exact unless
+            // it is below 2^-17 in magnitude or beyond fp16's range)
+            const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc[tb][r], u)) << 16);
+            hbase[dt * hw] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
+            bad = bad || !fp16_finite(hb);
+          }
+        }
+      if (bad && a.status) *a.status = MOE_ERR_RANGE;
+    }
+  } else {
+    float* obase = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row;
+#pragma unroll
+    for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) {
+        const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+        if (live && t0 + 4 * kh + dt < t1) obase[dt * R] = acc[tb][r];
+      }
+    // the other split slices of these rows (the combine adds every slice)
+    for (int sp = 1; sp < a.n_split_out; sp++) {
+      float* ob = obase + static_cast<int64_t>(sp) * a.split_stride;
+#pragma unroll
+      for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+          if (live && t0 + 4 * kh + dt < t1) ob[dt * R] = 0.f;
+        }
+    }
+  }
+}
+
+// Waves 0-3 take the gate rows and waves 4-7 the up rows of the tile's 128
+// positions, or all eight waves take 32 of the 256 down rows; a kind whose
+// class bit is set reads the 8-bit copies.
+template <int NM2, int NK, int B>
+__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0,
+                                              int pos1, int R, int t0, int t1) {
+  // the wave index through readfirstlane: the kind, the class bit and the
+  // buffer descriptors chosen by them are then scalar values, so no load is
+  // wrapped in a loop over the distinct descriptors of the wave's lanes
+  const int wv = uni(static_cast<int>(threadIdx.x >> 6));
+  const int kk = NK == 2 ? wv / 4 : 0;
+  const int rb = NK == 2 ? wv % 4 : wv;
+  const bool copy = (cls >> kk) & 1;
+  // the expert's base width: class 1 or 2 has one kind on copies, whose
+  // template width is 8 even though the base width is B.  The token tile of
+  // the item (an expert's last tile is partial) picks one, two or four
+  // 32-token blocks.
+  const int nt = t1 - t0;
+  if (nt <= 32) {
+    if (copy) tile_wave<NM2, NK, 8, 1>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+    else tile_wave<NM2, NK, B, 1>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  } else if (nt <= 64) {
+    if (copy) tile_wave<NM2, NK, 8, 2>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+    else tile_wave<NM2, NK, B, 2>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  } else {
+    if (copy) tile_wave<NM2, NK, 8, 4>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
+    else tile_wave<NM2, NK, B, 4>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+  }
+}
+
+// Eight waves, two per SIMD: a wave's 64 accumulator registers leave room for
+// a second wave, which hides the first one's load and LDS latencies.
+template <int NM2, int NK>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
+  __shared__ __attribute__((aligned(16))) HTile<NM2> tl;
+  __shared__ int pre[MOE_MAX_EXPERTS + 1];
+  for (int i = threadIdx.x; i <= map.n_e; i += blockDim.x) pre[i] = prefix[i];
+  __syncthreads();
+  const int total = pre[map.n_e];
+  const int G = gridDim.x;   // a multiple of kXcds
+  const int per = G / kXcds;
+  const int xcd = blockIdx.x % kXcds, loc = blockIdx.x / kXcds;
+  for (int it = 0;; it++) {
+    const int item = it * G + xcd * per + loc;
+    if (item >= total) break;
+    int lo = 0, hi = map.n_e - 1;   // last expert whose prefix is <= item
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (pre[mid] <= item) lo = mid; else hi = mid - 1;
+    }
+    const int e = map.e0 + lo;
+    const int local = item - pre[lo];
+    const int seg0 = uni(a.offsets[e]), seg1 = uni(a.offsets[e + 1]);
+    const int tiles = (seg1 - seg0 + kTileTok - 1) / kTileTok;
+    const bool routed = e < a.E;
+    const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
+    // (row block, token tile) of the local index: super-rows of kSuper row
+    // blocks, token tiles outer and row blocks inner within a super-row
+    int n_rb = 0;
+    if (routed) {
+      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) n_rb += (uni(cc[c]) + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
+    } else {
+      n_rb = (R + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
+    }
+    const int full = (n_rb / kSuper) * kSuper * tiles;
+    int rb, tt;
+    if (local < full) {
+      const int sr = local / (kSuper * tiles), rem = local - sr * kSuper * tiles;
+      tt = rem / kSuper;
+      rb = sr * kSuper + rem % kSuper;
+    } else {
+      const int h = n_rb % kSuper, rem = local - full;
+      tt = rem / h;
+      rb = (n_rb / kSuper) * kSuper + rem % h;
+    }
+    int cls = 0, start = 0, count = R;
+    if (routed) {
+      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
+      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) {
+        const int cn = uni(cc[c]);
+        const int nb = (cn + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
+        if (rb < nb) {
+          cls = c;
+          count = cn;
+          break;
+        }
+        rb -= nb;
+        start += cn;
+      }
+    }
+    const int pos0 = start + rb * kTileRowsOf<NK>;
+    const int pos1 = min(pos0 + kTileRowsOf<NK>, start + count);
+    const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
+    const int B = map.bits[e - map.e0];
+    if (B == 8) tile_dispatch<NM2, NK, 8>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if constexpr (NM2 % 4 == 0) {
+      if (B == 6) tile_dispatch<NM2, NK, 6>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+      else tile_dispatch<NM2, NK, 3>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    }
+    tile_barrier();   // the LDS stages are reused by the next item
+  }
+}
+
+// Instantiations: every group size by default; a build may compile this file
+// once per group size (MOE_FFN_NM = 2 or 4, that is 64 or 128).
+#if !defined(MOE_FFN_NM) || MOE_FFN_NM == 2
+template __global__ void tile_plan_kernel<1>(FfnArgs, TileMap, int32_t*);
+template __global__ void tile_plan_kernel<2>(FfnArgs, TileMap, int32_t*);
+template __global__ void ffn_tile_kernel<4, 1>(FfnArgs, TileMap, const int32_t*);
+template __global__ void ffn_tile_kernel<4, 2>(FfnArgs, TileMap, const int32_t*);
+#endif
+#if !defined(MOE_FFN_NM) || MOE_FFN_NM == 4
+template __global__ void ffn_tile_kernel<8, 1>(FfnArgs, TileMap, const int32_t*);
+template __global__ void ffn_tile_kernel<8, 2>(FfnArgs, TileMap, const int32_t*);
+#endif
+
+}  // namespace ffn
+}  // namespace moe

@@ -65,6 +65,7 @@ class MoELayer:
         self.bits = torch.tensor(self.bits_host, dtype=torch.int32, device=dev)
         self.router = torch.tensor(inputs.router, dtype=torch.float32, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.ffn_status = torch.zeros(1, dtype=torch.int32, device=dev)
         self._keep = []            # host arrays the descriptor points into
         self.kinds = []
         desc = LayerDesc()
@@ -234,7 +235,15 @@ class MoELayer:
 
     def ffn(self, x: torch.Tensor, b: Buffers, stream=None) -> None:
         api.moe_expert_ffn_mixed(self.desc, x, self.k, b.offsets, b.perm, b.o, b.ffn_ws,
-                                 stream=stream)
+                                 status=self.ffn_status, stream=stream)
+
+    def ffn_status_value(self) -> int:
+        """The FFN's device status word (0, or MOE_ERR_RANGE once the fp16
+        operand path has met a value beyond fp16's range); reads it back."""
+        return int(self.ffn_status.item())
+
+    def clear_ffn_status(self) -> None:
+        self.ffn_status.zero_()
 
     def combine(self, b: Buffers, stream=None) -> torch.Tensor:
         api.moe_unpermute_combine(b.o, b.n_split, b.inv, b.topk_w, self.k, self.S, b.y,

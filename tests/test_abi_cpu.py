@@ -150,18 +150,18 @@ def test_switch_and_ffn_validation(lib):
     assert ns.value >= 1 and wb.value > 0
     assert lib.moe_ffn_plan(C.byref(L), 16, 5, C.byref(ns), C.byref(wb)) == -1   # k > E
     f = lib.moe_expert_ffn_mixed
-    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value - 1, None) == -4
-    assert f(C.byref(L), MISALIGNED, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None) == -3
+    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value - 1, None, None) == -4
+    assert f(C.byref(L), MISALIGNED, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None, None) == -3
     L.d_ff = 500
-    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None) == -1
+    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None, None) == -1
     L.d_ff = 512
     # an empty batch: OK without touching any buffer (null activations, no workspace)
-    assert f(C.byref(L), None, 0, 2, None, None, None, None, 0, None) == 0
-    assert f(C.byref(L), None, -1, 2, None, None, None, None, 0, None) == -1
+    assert f(C.byref(L), None, 0, 2, None, None, None, None, 0, None, None) == 0
+    assert f(C.byref(L), None, -1, 2, None, None, None, None, 0, None, None) == -1
     bits = np.array([8, 4, 5, 2], np.int32)
     keep.append(bits)
     L.bits_host = bits.ctypes.data
-    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None) == -2
+    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None, None) == -2
 
 
 def test_requant_validation(lib):

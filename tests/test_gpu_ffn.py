@@ -101,22 +101,65 @@ def test_tiny_skewed_router_empty_experts(orc):
     assert rel_l2(y, res["y"]) <= 2e-4
 
 
-def _sampled_parity(orc, name, n_tok, seed=0):
+def segment_sample(offsets, perm, T, n_extra, seed):
+    """Tokens whose outputs are checked: for every expert segment (routed and
+    shared) the tokens of its first and last rows -- the last row sits in
+    the segment's partial tile -- plus n_extra tokens drawn at random.  The
+    segments come from the oracle's own routing."""
+    toks = set()
+    for e in range(len(offsets) - 1):
+        if offsets[e + 1] > offsets[e]:
+            toks.add(int(perm[offsets[e]]))
+            toks.add(int(perm[offsets[e + 1] - 1]))
+    rng = np.random.default_rng(seed)
+    toks.update(int(t) for t in rng.choice(T, size=min(n_extra, T), replace=False))
+    return np.array(sorted(toks), dtype=np.int64)
+
+
+def gpu_o_rows(b, rows):
+    """FFN output rows of the GPU (the sum of the split-K slices)."""
+    o = b.o[:, torch.as_tensor(rows, device=b.o.device)].double().sum(0)
+    return o.cpu().numpy()
+
+
+def check_segments(res, o_gpu, bound=TOL):
+    """Relative L2 of the expert outputs o over the checked rows of each
+    expert segment (each expert runs at its own precision, Sec. IV-A, so
+    every segment is held to the bound on its own).  Returns the worst."""
+    off, rows = res["offsets"], res["o_rows"]
+    worst = 0.0
+    for e in range(len(off) - 1):
+        sel = (rows >= off[e]) & (rows < off[e + 1])
+        if not np.any(sel):
+            continue
+        err = rel_l2(o_gpu[sel], res["o"][sel])
+        worst = max(worst, err)
+        assert err <= bound, "expert segment %d: rel L2 %.3g" % (e, err)
+    return worst
+
+
+def _sampled_parity(orc, name, n_extra, seed=0):
     wk, inp, layer = _layer(name)
     layer.set_epoch(0)
     rs = oracle_row_slots(orc, inp)
     batch = mi.make_batch(wk, inp)
     y, b = _run(layer, batch.x, batch.bias)
-    rng = np.random.default_rng(seed)
-    toks = np.sort(rng.choice(wk.tokens, size=min(n_tok, wk.tokens), replace=False))
-    print(name, "oracle on", len(toks), "tokens", flush=True)
+    _, ids, _ = orc.route(batch.x, inp.router, wk.layer.top_k, batch.bias)
+    off, perm, _ = orc.permute(ids, wk.layer.n_experts, wk.layer.n_shared)
+    toks = segment_sample(off, perm, wk.tokens, n_extra, seed)
+    print(name, "oracle on", len(toks), "tokens covering every expert segment", flush=True)
     res = orc.layer_forward(inp, batch.x, bias=batch.bias, row_slot=rs, tokens=toks)
     routing_matches(layer, res, b)
     for kd in range(3):
         assert np.array_equal(layer.row_slot(kd), rs[kd])
+    covered = {e for e in range(len(off) - 1)
+               if np.any((res["o_rows"] >= off[e]) & (res["o_rows"] < off[e + 1]))}
+    assert covered == {e for e in range(len(off) - 1) if off[e + 1] > off[e]}
+    seg = check_segments(res, gpu_o_rows(b, res["o_rows"]))
     err = rel_l2(y[toks], res["y"])
     per_tok = [rel_l2(y[t], res["y"][i]) for i, t in enumerate(toks)]
-    print(name, "rel_l2", err, "max per-token", max(per_tok), flush=True)
+    print(name, "rel_l2", err, "worst expert segment", seg, "max per-token", max(per_tok),
+          flush=True)
     assert err <= TOL
     assert max(per_tok) <= 1e-2
     return err
@@ -125,11 +168,11 @@ def _sampled_parity(orc, name, n_tok, seed=0):
 def test_deepseek_decode_parity(orc):
     # routed experts stream; the two shared experts see all 128 tokens and
     # stream too, their four 32-token tiles on separate workgroup sets
-    assert _sampled_parity(orc, "deepseek-decode", 48) <= DIAG_STREAM
+    assert _sampled_parity(orc, "deepseek-decode", 16) <= DIAG_STREAM
 
 
 def test_mixtral_decode_parity(orc):
-    assert _sampled_parity(orc, "mixtral-decode", 24) <= DIAG_STREAM
+    assert _sampled_parity(orc, "mixtral-decode", 16) <= DIAG_STREAM
 
 
 def test_ffn_run_to_run_deterministic():
@@ -144,41 +187,13 @@ def test_ffn_run_to_run_deterministic():
 
 def test_mixtral_prefill_parity(orc):
     # 4096 tokens, Zipf-skewed loads: experts with up to ~3300 rows, many
-    # 128-token tiles per expert
-    assert _sampled_parity(orc, "mixtral-prefill", 12) <= DIAG_TILE
+    # 128-token tiles per expert; every expert's first and last rows checked
+    assert _sampled_parity(orc, "mixtral-prefill", 16) <= DIAG_TILE
 
 
 def test_deepseek_prefill_parity(orc):
     # 8192 tokens, 64 routed experts + 2 shared experts over all tokens
-    assert _sampled_parity(orc, "deepseek-prefill", 12) <= DIAG_TILE
-
-
-def test_qwen_stress_mask_redraws(orc):
-    # fresh activations every step, the copy mask redrawn every 10 steps
-    wk = mi.WORKLOADS["qwen-stress"]
-    inp = mi.LayerInputs(wk.layer)
-    import paper_2503_21135_amd as P
-    layer = P.MoELayer(inp)
-    cache = {}
-    for step in (0, 10, 19):
-        epoch = step // wk.redraw_every
-        layer.set_epoch(epoch)
-        rs = oracle_row_slots(orc, inp, epoch=epoch)
-        for kd in range(3):
-            assert np.array_equal(layer.row_slot(kd), rs[kd])
-        batch = mi.make_batch(wk, inp, step=step)
-        y, b = _run(layer, batch.x, batch.bias)
-        toks = np.arange(0, wk.tokens, wk.tokens // 8)
-        key = ("epoch", epoch)
-        wc = cache.setdefault(key, {})
-        res = orc.layer_forward(inp, batch.x, bias=batch.bias, row_slot=rs, tokens=toks,
-                                weight_cache=wc)
-        routing_matches(layer, res, b)
-        err = rel_l2(y[toks], res["y"])
-        print("qwen step", step, "epoch", epoch, "switched %d%%" % inp.switch_percent(epoch),
-              "rel_l2", err, flush=True)
-        assert err <= TOL
-        assert err <= DIAG_STREAM   # ~34 tokens per routed expert, 512 on the shared one: all streamed
+    assert _sampled_parity(orc, "deepseek-prefill", 16) <= DIAG_TILE
 
 
 @pytest.mark.parametrize("T", [16, 40, 512])
@@ -273,3 +288,40 @@ def test_tile_sets_with_split_k(orc):
     err = rel_l2(y, res["y"])
     print("tile sets + split-K loads", np.diff(res["offsets"]).tolist(), "rel_l2", err, flush=True)
     assert err <= TOL and err <= DIAG_STREAM
+
+
+def test_fp16_operand_range_status(orc):
+    # The tile kernel (prefill sizes) multiplies fp16 copies of the
+    # activations and of h: a value with no finite fp16 value is reported
+    # through the FFN's status word (MOE_ERR_RANGE) rather than turned into
+    # infinities silently.  The streaming kernel (decode sizes) keeps bf16
+    # operands and is not affected.
+    from paper_2503_21135_amd import _lib
+    wk, inp, layer = _layer("tiny")
+    layer.set_epoch(0)
+    rs = oracle_row_slots(orc, inp)
+    T = 512   # 128 expected tokens per routed expert: the tile kernel
+    x = mi.make_x(wk.layer, T, stream=990)
+    layer.clear_ffn_status()
+    y, _ = _run(layer, x)
+    assert layer.ffn_status_value() == 0 and np.all(np.isfinite(y))
+    # one activation of 1e5 (a bf16 value, beyond fp16's 65504)
+    big = x.copy()
+    big[7, 3] = mi.bf16_bits(np.array([1e5], np.float32))[0]
+    layer.clear_ffn_status()
+    _run(layer, big)
+    assert layer.ffn_status_value() == _lib.ERR_RANGE
+    # the same batch at decode size streams with bf16 operands: no status,
+    # and the output matches the oracle
+    layer.clear_ffn_status()
+    y, b = _run(layer, big[:16])
+    assert layer.ffn_status_value() == 0
+    res = orc.layer_forward(inp, big[:16], row_slot=rs)
+    routing_matches(layer, res, b)
+    assert rel_l2(y, res["y"]) <= 2e-4
+    # activations inside fp16's range whose hidden values are not
+    xv = np.clip(mi.bf16_values(x).astype(np.float64) * 1000.0, -6e4, 6e4).astype(np.float32)
+    layer.clear_ffn_status()
+    _run(layer, mi.bf16_bits(xv))
+    assert layer.ffn_status_value() == _lib.ERR_RANGE
+    layer.clear_ffn_status()

@@ -230,3 +230,35 @@ def test_w3_switch_table(orc):
     st2, _ = orc.switch(hdr, 8, 512, layer.slots_on(0)[:5])
     st3, rs3 = orc.switch(hdr, 8, 512, on)
     assert np.array_equal(rs3, rs)
+
+
+def test_layer_weights_cache_matches_fresh_quantization(orc):
+    # the cached dequantized weights (used to check many steps) give each
+    # (expert, kind) exactly the matrix the oracle quantizes afresh, for
+    # several switch masks, and the same layer output bit for bit
+    wk = mi.WORKLOADS["tiny"]
+    inp = mi.LayerInputs(wk.layer)
+    lw = orc.LayerWeights(inp)
+    x = mi.make_x(wk.layer, 12, stream=321)
+    for epoch, slots in ((0, None), (0, "all")):
+        if slots is None:
+            rs = orc.switch_state(inp, epoch)
+        else:
+            rs = {}
+            for kd in range(3):
+                st, rs[kd] = orc.switch(inp.copy_headers(kd), wk.layer.n_experts,
+                                        wk.layer.rows(kd, 0),
+                                        np.arange(len(inp.copy_headers(kd)), dtype=np.int32))
+                assert st == 0
+        for e in range(wk.layer.n_experts):
+            for kd in range(3):
+                sw = np.nonzero(rs[kd][e] >= 0)[0]
+                ref = orc.effective_weight(inp.weight(e, kd), int(inp.bits[e]), wk.layer.group, sw)
+                assert np.array_equal(lw.effective(e, kd, sw), ref)
+        a = orc.layer_forward(inp, x, row_slot=rs)
+        b = orc.layer_forward(inp, x, row_slot=rs, weights=lw)
+        assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["o"], b["o"])
+        assert np.array_equal(a["o_rows"], np.arange(12 * wk.layer.top_k))
+    # a row without a cached copy cannot be switched
+    with pytest.raises(ValueError):
+        lw.effective(0, 0, np.array([wk.layer.d_ff + 5]))
