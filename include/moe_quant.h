@@ -29,7 +29,8 @@
  *     the compute-unit count of each device (read once per device, used to
  *     size the prefill grid), the MOE_DEBUG setting (read once), and
  *     per-thread scratch vectors that moe_set_channel_switch reuses for its
- *     host validation.
+ *     host validation.  moe_expert_ffn_mixed_noalloc additionally owns one
+ *     fixed device array per GPU (see there).
  *   - All device work is enqueued on `stream` (a hipStream_t, passed as void*;
  *     NULL is the default stream) and is asynchronous to the host.  No entry
  *     point reads device memory back to the host.
@@ -336,6 +337,34 @@ int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, int32_t T,
                             const int32_t* perm_token, float* o,
                             void* ws, size_t ws_bytes, int32_t* status, void* stream,
                             void* const* events, int32_t n_events);
+
+/*
+ * moe_expert_ffn_mixed_noalloc -- moe_expert_ffn_mixed without a workspace
+ * argument, for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  It
+ * calls no hipMalloc, hipFree or allocating library routine.
+ *
+ * Its workspace is one fixed device array of MOE_NOALLOC_SCRATCH_BYTES (64
+ * MiB) per GPU, part of the library's code object: each GPU the library runs
+ * on holds it until the process ends.  Its device address is looked up once
+ * per device, on the first call made with that device current.  Batches
+ * whose workspace (moe_ffn_plan's ws_bytes) exceeds the array are rejected
+ * with MOE_ERR_WORKSPACE before any device work: decode and mid-size batches
+ * fit (the Mixtral-shaped layer at 64 tokens needs ~4 MB, the Qwen-shaped
+ * layer at 512 tokens ~12 MB), prefill batches of thousands of tokens use
+ * moe_expert_ffn_mixed with a caller workspace.  Nothing in the array needs
+ * to start at zero.  Every call on one GPU shares that GPU's array: calls
+ * that overlap in time on one GPU (different streams, or different host
+ * threads without ordering) race and give undefined results; calls ordered
+ * on one stream do not.  Same arguments (minus ws, ws_bytes), results and
+ * errors as moe_expert_ffn_mixed otherwise; MOE_ERR_HIP if the array's
+ * address cannot be obtained.
+ */
+#define MOE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int moe_expert_ffn_mixed_noalloc(const moe_layer_t* L, const uint16_t* x, int32_t T,
+                                 int32_t k, const int32_t* offsets,
+                                 const int32_t* perm_token, float* o,
+                                 int32_t* status, void* stream);
 
 /*
  * moe_set_channel_switch -- install a set of cached copies.

@@ -16,11 +16,13 @@ OK, ERR_ARG, ERR_BITS, ERR_ALIGN, ERR_WORKSPACE, ERR_SLOT, ERR_RANGE, ERR_HIP = 
 KIND_GATE, KIND_UP, KIND_DOWN = 0, 1, 2
 MAX_EXPERTS = 256
 MAX_TOPK = 16
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 EXPORTS = (
     "moe_quant_pack", "moe_code_row_words", "moe_route_permute", "moe_route_workspace_bytes",
     "moe_ffn_plan",
-    "moe_expert_ffn_mixed", "moe_expert_ffn_mixed_ev", "moe_set_channel_switch",
+    "moe_expert_ffn_mixed", "moe_expert_ffn_mixed_ev", "moe_expert_ffn_mixed_noalloc",
+    "moe_set_channel_switch",
     "moe_requant_channels", "moe_unpermute_combine", "moe_status_str",
     "moe_expert_significance", "moe_allocate_bits",
 )
@@ -74,6 +76,8 @@ def load() -> C.CDLL:
                                            sz_t, vp, vp]),
         "moe_expert_ffn_mixed_ev": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp, vp,
                                               sz_t, vp, vp, vp, i32]),
+        "moe_expert_ffn_mixed_noalloc": (C.c_int, [C.POINTER(LayerDesc), vp, i32, i32, vp, vp, vp,
+                                                   vp, vp]),
         "moe_set_channel_switch": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i32, vp]),
         "moe_requant_channels": (C.c_int, [C.POINTER(LayerDesc), i32, vp, i64, vp, vp, vp]),
         "moe_unpermute_combine": (C.c_int, [vp, i32, i64, vp, vp, i32, i32, i32, i32, vp, vp]),

@@ -111,6 +111,18 @@ def moe_expert_ffn_mixed_ev(desc: LayerDesc, x: torch.Tensor, k: int, offsets: t
     check(st, "moe_expert_ffn_mixed_ev")
 
 
+def moe_expert_ffn_mixed_noalloc(desc: LayerDesc, x: torch.Tensor, k: int, offsets: torch.Tensor,
+                                 perm_token: torch.Tensor, o: torch.Tensor,
+                                 status: Optional[torch.Tensor] = None, stream=None) -> None:
+    """moe_expert_ffn_mixed with the library's fixed per-GPU workspace
+    (no workspace argument, no allocation)."""
+    _need_cuda(x, offsets, perm_token, o, status)
+    T = x.shape[0]
+    st = load().moe_expert_ffn_mixed_noalloc(C.byref(desc), _p(x), T, k, _p(offsets),
+                                             _p(perm_token), _p(o), _p(status), _s(stream))
+    check(st, "moe_expert_ffn_mixed_noalloc")
+
+
 def moe_set_channel_switch(desc: LayerDesc, kind: int, slots_on: Optional[np.ndarray],
                            stream=None) -> None:
     """Install cached copies by (expert, row) header (Sec. IV-B, V-A)."""

@@ -4,6 +4,7 @@
 // ffn_stream.hip and ffn_tile.hip.
 #include <algorithm>
 #include <functional>
+#include <mutex>
 #include <type_traits>
 #include <vector>
 
@@ -417,4 +418,49 @@ extern "C" int moe_expert_ffn_mixed_ev(const moe_layer_t* L, const uint16_t* x, 
   if (n_events < 0 || (n_events > 0 && !events)) return MOE_ERR_ARG;
   return moe::ffn::ffn_entry(L, x, T, k, offsets, perm_token, o, ws, ws_bytes, status, stream, events,
                         n_events);
+}
+
+// ------------------------------------------------------------------ no-allocation variant
+// The workspace of moe_expert_ffn_mixed_noalloc: one fixed array per GPU,
+// loaded with the library's code object, so the call needs no allocation.
+// Host code never uses the array's name as an address (on the host it is a
+// stand-in, not the device address): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[MOE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {nullptr};
+
+// Device address of this device's scratch array, or null on failure.
+void* scratch_address() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" int moe_expert_ffn_mixed_noalloc(const moe_layer_t* L, const uint16_t* x, int32_t T,
+                                            int32_t k, const int32_t* offsets,
+                                            const int32_t* perm_token, float* o, int32_t* status,
+                                            void* stream) {
+  using namespace moe::ffn;
+  int st = validate_layer(L);
+  if (st != MOE_OK) return st;
+  if (T < 0 || k < 1 || k > L->n_experts || k > MOE_MAX_TOPK) return MOE_ERR_ARG;
+  if (T == 0) return MOE_OK;
+  const Plan p = make_plan(L, T, k);
+  // the plan's workspace (already including its 256 bytes of alignment slack)
+  // must fit the fixed array
+  if (p.total > static_cast<size_t>(MOE_NOALLOC_SCRATCH_BYTES)) return MOE_ERR_WORKSPACE;
+  void* ws = scratch_address();
+  if (!ws) return MOE_ERR_HIP;
+  return moe::ffn::ffn_entry(L, x, T, k, offsets, perm_token, o, ws, MOE_NOALLOC_SCRATCH_BYTES, status,
+                             stream, nullptr, 0);
 }

@@ -158,10 +158,24 @@ def test_switch_and_ffn_validation(lib):
     # an empty batch: OK without touching any buffer (null activations, no workspace)
     assert f(C.byref(L), None, 0, 2, None, None, None, None, 0, None, None) == 0
     assert f(C.byref(L), None, -1, 2, None, None, None, None, 0, None, None) == -1
+    # the no-allocation variant: an empty batch needs nothing; a batch whose
+    # workspace exceeds the fixed per-GPU array is refused before any device work
+    na = lib.moe_expert_ffn_mixed_noalloc
+    assert na(C.byref(L), None, 0, 2, None, None, None, None, None) == 0
+    assert na(C.byref(L), None, -1, 2, None, None, None, None, None) == -1
+    from paper_2503_21135_amd import _lib
+    T = 16
+    while True:
+        assert lib.moe_ffn_plan(C.byref(L), T, 2, C.byref(ns), C.byref(wb)) == 0
+        if wb.value > _lib.NOALLOC_SCRATCH_BYTES:
+            break
+        T *= 2
+    assert na(C.byref(L), FAKE, T, 2, FAKE, FAKE, FAKE, None, None) == -4
     bits = np.array([8, 4, 5, 2], np.int32)
     keep.append(bits)
     L.bits_host = bits.ctypes.data
     assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None, None) == -2
+    assert na(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, None, None) == -2
 
 
 def test_requant_validation(lib):
