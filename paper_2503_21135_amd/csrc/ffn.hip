@@ -122,53 +122,67 @@ int validate_layer(const moe_layer_t* L) {
   return MOE_OK;
 }
 
-// Work map of one launch (routed experts, or the shared experts).  The
-// switched-class workgroups per routed expert bound what its copies can need:
-// classes 1..3 of gate/up hold at most n_gate + n_up rows in three classes,
-// class 1 of down at most n_down rows.
-WgMap stream_map(const moe_layer_t* L, bool shared, bool down) {
+// Work map of the streaming launch of one stage, over the routed experts
+// (routed) and/or the shared experts (shared).  The switched-class
+// workgroups per routed expert bound what its copies can need: classes 1..3
+// of gate/up hold at most n_gate + n_up rows in three classes, class 1 of
+// down at most n_down rows.  Class-0 entries: shared experts first, then
+// the routed experts widest first.
+WgMap stream_map(const moe_layer_t* L, const Plan& p, bool routed, bool shared, bool down, int n_split) {
   WgMap m{};
-  const int rows = (down ? kWavesOf<1> : kWavesOf<2>) * 16;
-  const int E = L->n_experts;
-  if (shared) {
-    m.e0 = E;
-    m.n_e = L->n_shared;
-    m.n_sw = 0;
-    m.per_e = (down ? L->d_model : L->d_ff_shared) / rows;
-    for (int i = 0; i < L->n_shared; i++) {
-      m.order[i] = static_cast<int16_t>(i);
-      m.bits[i] = static_cast<int8_t>(L->bits_host[E + i]);
+  const int rows1 = (down ? kWavesOf<1> : kWavesOf<2>) * 16;
+  const int E = L->n_experts, S = L->n_shared;
+  m.n_split = n_split;
+  m.tt_r = std::max(p.tt_routed, 1);
+  m.tt_s = std::max(p.tt_shared, 1);
+  m.m_r = m.tt_r * n_split;
+  m.m_s = m.tt_s * n_split;
+  for (int e = 0; e < E + S; e++) m.bits[e] = static_cast<int8_t>(L->bits_host[e]);
+  if (routed) {
+    const int R = down ? L->d_model : L->d_ff;
+    std::vector<int> nc[2];
+    for (int kk = 0; kk < (down ? 1 : 2); kk++) {
+      const moe_kind_desc_t& k = L->kind[down ? 2 : kk];
+      nc[kk].assign(E, 0);
+      for (int s = 0; s < k.n_slots; s++) {
+        const int e = k.copy_hdr_host ? k.copy_hdr_host[2 * s] : -1;
+        if (e >= 0 && e < E) nc[kk][e]++;
+        else std::fill(nc[kk].begin(), nc[kk].end(), R);   // headers unknown: any row
+      }
+      for (int e = 0; e < E; e++) nc[kk][e] = std::min(nc[kk][e], R);
     }
-    return m;
-  }
-  const int R = down ? L->d_model : L->d_ff;
-  m.e0 = 0;
-  m.n_e = E;
-  m.per_e = R / rows;
-  std::vector<int> nc[2];
-  for (int kk = 0; kk < (down ? 1 : 2); kk++) {
-    const moe_kind_desc_t& k = L->kind[down ? 2 : kk];
-    nc[kk].assign(E, 0);
-    for (int s = 0; s < k.n_slots; s++) {
-      const int e = k.copy_hdr_host ? k.copy_hdr_host[2 * s] : -1;
-      if (e >= 0 && e < E) nc[kk][e]++;
-      else std::fill(nc[kk].begin(), nc[kk].end(), R);   // headers unknown: any row
+    int n_sw = 0;
+    for (int e = 0; e < E; e++) {
+      const int64_t need = down ? cdiv(nc[0][e], rows1)
+                                : (nc[0][e] + nc[1][e] > 0 ? cdiv(nc[0][e] + nc[1][e], rows1) + 2 : 0);
+      n_sw = std::max<int>(n_sw, static_cast<int>(std::min<int64_t>(need, cdiv(R, rows1) + 3)));
     }
-    for (int e = 0; e < E; e++) nc[kk][e] = std::min(nc[kk][e], R);
+    m.n_r = n_sw > 0 ? E : 0;
+    m.n_sw = n_sw;
   }
-  int n_sw = 0;
-  for (int e = 0; e < E; e++) {
-    const int64_t need = down ? cdiv(nc[0][e], rows)
-                              : (nc[0][e] + nc[1][e] > 0 ? cdiv(nc[0][e] + nc[1][e], rows) + 2 : 0);
-    n_sw = std::max<int>(n_sw, static_cast<int>(std::min<int64_t>(need, cdiv(R, rows) + 3)));
-  }
-  m.n_sw = n_sw;
-  for (int e = 0; e < E; e++) m.bits[e] = static_cast<int8_t>(L->bits_host[e]);
   int n = 0;
-  for (int b : {8, 6, 4, 3, 2})
-    for (int e = 0; e < E; e++)
-      if (L->bits_host[e] == b) m.order[n++] = static_cast<int16_t>(e);
+  int32_t start = 0;
+  auto entry = [&](int e) {
+    const int R = down ? L->d_model : (e < E ? L->d_ff : L->d_ff_shared);
+    const int64_t nblk = cdiv(R, rows1 * stream_rt(L->bits_host[e]));
+    m.ent_e[n] = static_cast<int16_t>(e);
+    m.ent_start[n] = start;
+    start += static_cast<int32_t>(nblk * (e < E ? m.m_r : m.m_s));
+    n++;
+  };
+  if (shared)
+    for (int s = 0; s < S; s++) entry(E + s);
+  if (routed)
+    for (int b : {8, 6, 4, 3, 2})
+      for (int e = 0; e < E; e++)
+        if (L->bits_host[e] == b) entry(e);
+  m.ent_start[n] = start;
+  m.n_ent = n;
   return m;
+}
+
+int64_t stream_grid(const WgMap& m) {
+  return static_cast<int64_t>(m.n_r) * m.n_sw * m.m_r + (m.n_ent > 0 ? m.ent_start[m.n_ent] : 0);
 }
 
 TileMap tile_map(const moe_layer_t* L, bool shared) {
@@ -250,37 +264,42 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     if (S > 0) prep(a.Tk, a.rows, p.nt_shared == 0);
   }
   int32_t* prefix = a.tile_prefix;
-  auto add = [&](std::vector<Launch>& v, auto nk, bool shared, int nt, int nsplit) {
+  // tile path: plan kernel, then the persistent tile kernel, for one expert set
+  auto add_tile = [&](std::vector<Launch>& v, auto nk, bool shared) {
     constexpr int NK = decltype(nk)::value;
-    if (nt == 0) {  // tile path: plan kernel, then the persistent tile kernel
-      const TileMap m = tile_map(L, shared);
-      const int32_t* pf = prefix;
-      prefix += MOE_MAX_EXPERTS + 1;
-      if (m.n_e == 0) return;
-      v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-        klaunch(tile_plan_kernel<NK>, dim3(1), dim3(256), s, e0, e1, a, m, const_cast<int32_t*>(pf));
-      });
-      v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-        klaunch(ffn_tile_kernel<2 * NM, NK>, dim3(static_cast<unsigned>(tile_grid())), dim3(64 * kTileWaves), s,
-                e0, e1, a, m, pf);
-      });
-      return;
-    }
-    const WgMap m = stream_map(L, shared, NK == 1);
-    const int64_t n_wg = static_cast<int64_t>(m.n_e) * (m.n_sw + m.per_e);
+    const TileMap m = tile_map(L, shared);
+    const int32_t* pf = prefix;
+    prefix += MOE_MAX_EXPERTS + 1;
+    if (m.n_e == 0) return;
+    v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+      klaunch(tile_plan_kernel<NK>, dim3(1), dim3(256), s, e0, e1, a, m, const_cast<int32_t*>(pf));
+    });
+    v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+      klaunch(ffn_tile_kernel<2 * NM, NK>, dim3(static_cast<unsigned>(tile_grid())), dim3(64 * kTileWaves), s,
+              e0, e1, a, m, pf);
+    });
+  };
+  // streaming path: one launch for every expert set that streams
+  auto add_stream = [&](std::vector<Launch>& v, auto nk, int nsplit) {
+    constexpr int NK = decltype(nk)::value;
+    const bool r = p.nt_routed != 0, sh = S > 0 && p.nt_shared != 0;
+    if (!r && !sh) return;
+    const WgMap m = stream_map(L, p, r, sh, NK == 1, nsplit);
+    const int64_t n_wg = stream_grid(m);
     if (n_wg == 0) return;
-    const int n_tt = shared ? p.tt_shared : p.tt_routed;
-    const dim3 grid(static_cast<unsigned>(n_wg * nsplit * n_tt));
+    const int nt = std::max(r ? p.nt_routed : 0, sh ? p.nt_shared : 0);
+    const dim3 grid(static_cast<unsigned>(n_wg));
     v.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
       const dim3 block(64 * kWavesOf<NK>);
-      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, block, s, e0, e1, a, m, nsplit, n_tt);
-      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, block, s, e0, e1, a, m, nsplit, n_tt);
+      if (nt == 1) klaunch(ffn_stream_kernel<NM, 1, NK>, grid, block, s, e0, e1, a, m);
+      else klaunch(ffn_stream_kernel<NM, 2, NK>, grid, block, s, e0, e1, a, m);
     });
   };
   using two = std::integral_constant<int, 2>;
   using one = std::integral_constant<int, 1>;
-  add(gate_up, two{}, false, p.nt_routed, 1);
-  if (S > 0) add(gate_up, two{}, true, p.nt_shared, 1);
+  if (p.nt_routed == 0) add_tile(gate_up, two{}, false);
+  if (S > 0 && p.nt_shared == 0) add_tile(gate_up, two{}, true);
+  add_stream(gate_up, two{}, 1);
   {  // group sums of h, [max(f,fs)/g][rows], for the rows the streaming kernel reads
     // (routed rows f wide, shared rows fs wide; one launch when both stream)
     auto hs = [&](int p0, int p1) {
@@ -296,8 +315,9 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     else if (rs) hs(0, a.Tk);
     else if (ss) hs(a.Tk, a.rows);
   }
-  add(down, one{}, false, p.nt_routed, p.n_split);
-  if (S > 0) add(down, one{}, true, p.nt_shared, p.n_split);
+  if (p.nt_routed == 0) add_tile(down, one{}, false);
+  if (S > 0 && p.nt_shared == 0) add_tile(down, one{}, true);
+  add_stream(down, one{}, p.n_split);
   issue(xsum, event(0), nullptr, s);
   issue(gate_up, event(1), event(2), s);
   issue(hsum, nullptr, nullptr, s);

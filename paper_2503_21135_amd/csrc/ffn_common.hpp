@@ -258,18 +258,28 @@ __device__ __forceinline__ void lds_dma16(Rsrc r, void* lds, uint32_t off, uint3
 template <int NK>
 constexpr int kWavesOf = NK == 1 ? 8 : 4;
 
-// Work of one launch over experts e0 .. e0+n_e-1.  Every workgroup covers
-// kWavesOf<NK>*16 row positions of one source class of one expert.  Workgroups
-// [0, n_e*n_sw) take the switched classes (n_sw per expert, an upper bound
-// on what its copies can need; those beyond the expert's actual class sizes
-// exit at once); the rest take class 0, per_e workgroups per expert, experts
-// in the order `order` (widest bit-width first).
+// Row tiles of 16 rows per wave for a class whose rows all read base codes
+// of width b, shared by the kernel and the host's work map.  Measured on
+// MI355X: two row tiles per wave at 3 and 4 bits and three at 2 bits
+// (workgroups streaming about as many bytes as an 8-bit one) left a layer of
+// one width unchanged and the mixed layers slower (fewer, equal workgroups
+// leave a partial last round), so every width takes one.
+__host__ __device__ constexpr int stream_rt(int b) { return b > 0 ? 1 : 1; }
+
+// Work map of one streaming launch.  Workgroups [0, n_r*n_sw*m_r) take the
+// switched classes of routed experts 0..n_r-1 (n_sw row blocks of one row
+// tile per wave per expert, m_r variants each); the rest are the class-0
+// row blocks of the entries ent_e[0..n_ent), entry i owning workgroups
+// [ent_start[i], ent_start[i+1]) after the switched section: its row blocks
+// (kWavesOf<NK> * 16 * stream_rt(bits) rows each) times its variants (m_r
+// for routed, m_s for shared experts).  A variant is a token-tile set
+// (tt_r / tt_s sets, each taking every n-th 32-token tile of the expert)
+// and a K slice (n_split).
 struct WgMap {
-  int e0, n_e;
-  int n_sw;
-  int per_e;
-  int16_t order[MOE_MAX_EXPERTS];
-  int8_t bits[MOE_MAX_EXPERTS];   // bits[e - e0]
+  int n_r, n_sw, m_r, m_s, tt_r, tt_s, n_split, n_ent;
+  int32_t ent_start[MOE_MAX_EXPERTS + 1];
+  int16_t ent_e[MOE_MAX_EXPERTS];
+  int8_t bits[MOE_MAX_EXPERTS];   // bit-width of expert e (routed and shared)
 };
 
 constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token blocks)
@@ -295,7 +305,7 @@ struct TileMap {
 // ffn.hip.
 template <int NM, int NT, int NK>
 __global__ void __launch_bounds__(64 * kWavesOf<NK>) __attribute__((amdgpu_waves_per_eu(2)))
-ffn_stream_kernel(FfnArgs a, WgMap map, int n_split, int n_tt);
+ffn_stream_kernel(FfnArgs a, WgMap map);
 
 template <int NM>
 __global__ void __launch_bounds__(256)

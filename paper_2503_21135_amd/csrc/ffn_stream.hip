@@ -42,7 +42,7 @@ namespace ffn {
 // source for all rows -- the expert's base codes at bit-width B, or the
 // cached 8-bit copies -- so the loads are wave-uniform in shape and the code
 // registers are sized for that width (template BG / BU).  The packed codes of
-// the next kStages<BG, BU> groups are in flight in registers while the current group
+// the next kStages<RT, BG, BU> groups are in flight in registers while the current group
 // is dequantized and contracted; the activations of the workgroup's token
 // tile (NT*16 rows) are staged in LDS two groups at a time (double-buffered,
 // one barrier per two groups), so every wave reads them from LDS.
@@ -53,8 +53,10 @@ namespace ffn {
 // them (vector loads complete in order) never waits for a code load the loop
 // does not already need: with two-group chunks that holds for up to four
 // groups in flight.
-template <int BG, int BU>
-constexpr int kStages = (BG == 8 || BU == 8 || BG == 6 || BU == 6) ? 2 : 4;
+// With two or four row tiles per wave (narrow codes) two groups in flight
+// already hold as many bytes as four groups of one row tile.
+template <int RT, int BG, int BU>
+constexpr int kStages = (RT >= 2 || BG == 8 || BU == 8 || BG == 6 || BU == 6) ? 2 : 4;
 
 
 // Metadata a workgroup loads in its prologue, all issued before any is
@@ -62,7 +64,6 @@ constexpr int kStages = (BG == 8 || BU == 8 || BG == 6 || BU == 6) ? 2 : 4;
 // costs more than the loads themselves).
 struct Pre {
   int64_t code_off[2], sz_off[2];   // per kind of the launch
-  int row0;                         // class 0: this lane's row of the order
   int tt, n_tt;                     // token tile of the workgroup, when the tiles are split over workgroups
 };
 
@@ -150,31 +151,39 @@ __device__ __forceinline__ void contract_kind(const uint32_t (&cw)[(kWords<NM, B
   }
 }
 
+// The row tiles of a wave are contracted in turn, software-pipelined: the
+// MFMAs of row tile rt are issued before the scale/zero epilogue of tile
+// rt - 1, so the matrix cores work on one tile while the epilogue of the
+// previous one runs, and only two tiles' partial sums are live at once.
 template <int NM, int NT, int RT, int NK, int BG, int BU>
 __device__ __forceinline__ void compute_group(const Stage<NM, RT, BG, BU>& st, const uint32_t (&szw)[RT][2],
                                               const u32x4 (&af)[NT][NM], const f32x4 (&X)[NT],
                                               uint32_t vm, uint32_t vh, f32x4 (&acc)[RT][NK][NT]) {
-  f32x4 tmp[RT][NK][NT];
-  float sc[RT][NK], zz[RT][NK];
+  f32x4 tmp[2][NK][NT];
+  float sc[2][NK], zz[2][NK];
 #pragma unroll
-  for (int rt = 0; rt < RT; rt++) {
-    contract_kind<NM, NT, BG>(st.cg[rt], szw[rt][0], af, vm, vh, tmp[rt][0], sc[rt][0], zz[rt][0]);
-    if constexpr (NK == 2)
-      contract_kind<NM, NT, BU>(st.cu[rt], szw[rt][1], af, vm, vh, tmp[rt][1], sc[rt][1], zz[rt][1]);
+  for (int rt = 0; rt <= RT; rt++) {
+    if (rt < RT) {
+      const int b = rt & 1;
+      contract_kind<NM, NT, BG>(st.cg[rt], szw[rt][0], af, vm, vh, tmp[b][0], sc[b][0], zz[b][0]);
+      if constexpr (NK == 2)
+        contract_kind<NM, NT, BU>(st.cu[rt], szw[rt][1], af, vm, vh, tmp[b][1], sc[b][1], zz[b][1]);
+    }
+    if (rt > 0) {
+      const int b = (rt - 1) & 1;
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++)
+#pragma unroll
+        for (int nt = 0; nt < NT; nt++)
+#pragma unroll
+          for (int i = 0; i < 4; i++)
+            acc[rt - 1][kk][nt][i] = __fmaf_rn(sc[b][kk], __fmaf_rn(-zz[b][kk], X[nt][i], tmp[b][kk][nt][i]),
+                                               acc[rt - 1][kk][nt][i]);
+    }
   }
-  __builtin_amdgcn_sched_barrier(0);
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int rt = 0; rt < RT; rt++)
-#pragma unroll
-    for (int kk = 0; kk < NK; kk++)
-#pragma unroll
-      for (int nt = 0; nt < NT; nt++)
-#pragma unroll
-        for (int i = 0; i < 4; i++)
-          acc[rt][kk][nt][i] = __fmaf_rn(sc[rt][kk], __fmaf_rn(-zz[rt][kk], X[nt][i], tmp[rt][kk][nt][i]),
-                                         acc[rt][kk][nt][i]);
 }
 
 // Groups per LDS chunk of activations.  (Four-group chunks halve the
@@ -206,7 +215,7 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
   constexpr int PIECES = TOK * KC / 8;   // 16-byte pieces per chunk
   constexpr int PPT = (PIECES + kThreads - 1) / kThreads;
   static_assert(PIECES % kThreads == 0 || PIECES < kThreads, "chunk must split evenly over the workgroup");
-  constexpr int S = kStages<BG, BU>;
+  constexpr int S = kStages<RT, BG, BU>;
   constexpr int CG = XTile<NM, NT>::CG;
   static_assert((S == 2 || S == 4) && CG == 2, "the loop body below handles two two-group chunks");
   static_assert(CG * TOK <= kThreads, "one thread per group-sum entry of a chunk");
@@ -235,10 +244,13 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
     live[rt] = pos < pos1;
     // positions past the class (pos >= pos1) are not read: for the last
     // expert's last class they would lie past the end of the order table
-    const int prow = (RT == 1 && cls == 0) ? pre.row0
-                                            : ((live[rt] && routed) ? order[static_cast<int64_t>(e) * R + pos] : 0);
+    const int prow = (live[rt] && routed) ? order[static_cast<int64_t>(e) * R + pos] : 0;
     row_id[rt] = live[rt] ? (routed ? prow : pos) : 0;
   }
+  // a wave whose rows all lie past the class (the last workgroup of an
+  // expert whose rows do not fill it) still stages activations and meets the
+  // barriers, but contracts nothing
+  const bool wave_live = uni(pos0 + wv * 16 * RT) < pos1;
   Src<RT> src[2];
 #pragma unroll
   for (int kk = 0; kk < NK; kk++) {
@@ -336,7 +348,7 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
     if constexpr (CG == 2) stage_x(vx[1], vxs[1], g0 + 2);
     __syncthreads();
     auto group = [&](Stage<NM, RT, BG, BU>& s, int buf, int gg, int gi, int i4) {
-      if (gi < g1) {   // wave-uniform; the loads below are unconditional
+      if (gi < g1 && wave_live) {   // wave-uniform; the loads below are unconditional
         uint32_t szw[RT][2];
 #pragma unroll
         for (int rt = 0; rt < RT; rt++)
@@ -403,44 +415,71 @@ __device__ __forceinline__ void stream_body(const FfnArgs& a, XTile<NM, NT>& tl,
 }
 
 
+// Class 0 (both kinds on the expert's base codes) takes stream_rt(B) row
+// tiles per wave; the switched classes (one or both kinds on the 8-bit
+// copies) one.
 template <int NM, int NT, int NK, int B>
 __device__ __forceinline__ void dispatch_class(const FfnArgs& a, XTile<NM, NT>& tl, const Pre& pre, int e,
                                                int cls, int pos0, int pos1, int R, int sp, int n_split) {
+  constexpr int RT0 = stream_rt(B);
   if constexpr (NK == 1) {
-    if (cls == 0) stream_body<NM, NT, 1, 1, B, B>(a, tl, pre, e, 0, pos0, pos1, R, sp, n_split);
+    if (cls == 0) stream_body<NM, NT, RT0, 1, B, B>(a, tl, pre, e, 0, pos0, pos1, R, sp, n_split);
     else stream_body<NM, NT, 1, 1, 8, 8>(a, tl, pre, e, 1, pos0, pos1, R, sp, n_split);
   } else {
-    if (cls == 0) stream_body<NM, NT, 1, 2, B, B>(a, tl, pre, e, 0, pos0, pos1, R, sp, n_split);
+    if (cls == 0) stream_body<NM, NT, RT0, 2, B, B>(a, tl, pre, e, 0, pos0, pos1, R, sp, n_split);
     else if (cls == 1) stream_body<NM, NT, 1, 2, 8, B>(a, tl, pre, e, 1, pos0, pos1, R, sp, n_split);
     else if (cls == 2) stream_body<NM, NT, 1, 2, B, 8>(a, tl, pre, e, 2, pos0, pos1, R, sp, n_split);
     else stream_body<NM, NT, 1, 2, 8, 8>(a, tl, pre, e, 3, pos0, pos1, R, sp, n_split);
   }
 }
 
-// One launch serves every class of a set of experts: the switched-class
-// workgroups come first in the grid, then the class-0 workgroups, widest
-// bit-width first.
+// Local index l of a workgroup inside a run of nblk row blocks with m
+// variants each (token-tile sets x K slices) -> (block, variant).  Blocks
+// go in chunks of 8 with the variant outside the block inside a chunk, so
+// the variants of one block are 8 workgroups apart: the hardware places
+// workgroup b on XCD b % 8, so they run on one XCD and share its L2 (the
+// block's codes are read from HBM once).
+__device__ __forceinline__ void block_variant(int l, int nblk, int m, int& blk, int& v) {
+  const int c = l / (8 * m);
+  const int r = l - c * 8 * m;
+  const int nb = min(8, nblk - 8 * c);
+  v = r / nb;
+  blk = 8 * c + (r - v * nb);
+}
+
+// One launch serves every streamed expert of a stage: the switched-class
+// workgroups of the routed experts first (n_sw per expert, an upper bound on
+// what its copies can need; those past its actual class sizes exit at once),
+// then the class-0 workgroups of the entries of the map (shared experts,
+// then routed experts widest first), each entry's row blocks sized by its
+// bit-width so that every workgroup streams about the same bytes.
 template <int NM, int NT, int NK>
 __global__ void __launch_bounds__(64 * kWavesOf<NK>) __attribute__((amdgpu_waves_per_eu(2)))
-ffn_stream_kernel(FfnArgs a, WgMap map, int n_split, int n_tt) {
+ffn_stream_kernel(FfnArgs a, WgMap map) {
   __shared__ __attribute__((aligned(16))) XTile<NM, NT> tl;
-  constexpr int rows = kWavesOf<NK> * 16;
-  const int tt = blockIdx.x % n_tt;
-  const int wgi = blockIdx.x / n_tt / n_split;
-  const int sp = blockIdx.x / n_tt % n_split;
-  const int n_swg = map.n_e * map.n_sw;
-  int e, cls, blk;
-  if (wgi < n_swg) {
-    e = map.e0 + wgi / map.n_sw;
-    blk = wgi % map.n_sw;
-    cls = 0;
+  constexpr int rows1 = kWavesOf<NK> * 16;   // rows of one row tile per wave
+  const int bid = blockIdx.x;
+  const int n_swg = map.n_r * map.n_sw * map.m_r;
+  int e, blk, v;
+  const bool sw = bid < n_swg;
+  if (sw) {
+    const int per = map.n_sw * map.m_r;
+    e = bid / per;
+    block_variant(bid - e * per, map.n_sw, map.m_r, blk, v);
   } else {
-    const int j = wgi - n_swg;
-    e = map.e0 + map.order[j / map.per_e];
-    blk = j % map.per_e;
-    cls = 0;
+    const int w = bid - n_swg;
+    int lo = 0, hi = map.n_ent - 1;   // last entry whose start is <= w
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (map.ent_start[mid] <= w) lo = mid; else hi = mid - 1;
+    }
+    e = map.ent_e[lo];
+    const int m = e < a.E ? map.m_r : map.m_s;
+    block_variant(w - map.ent_start[lo], (map.ent_start[lo + 1] - map.ent_start[lo]) / m, m, blk, v);
   }
   const bool routed = e < a.E;
+  const int n_tt = routed ? map.tt_r : map.tt_s;
+  const int tt = v % n_tt, sp = v / n_tt;
   const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
   const int kind0 = NK == 1 ? 2 : 0;
   // issue every metadata load of the workgroup before waiting for any of them
@@ -457,16 +496,15 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split, int n_tt) {
     pre.code_off[kk] = a.kd[kind0 + kk].code_off[e];
     pre.sz_off[kk] = a.kd[kind0 + kk].sz_off[e];
   }
-  const int32_t* order = NK == 1 ? a.order_dn : a.order_gu;
-  pre.row0 = (routed && wgi >= n_swg)
-                 ? order[static_cast<int64_t>(e) * R + blk * rows + (threadIdx.x >> 6) * 16 + (threadIdx.x & 15)]
-                 : 0;
   if (uni(o1) <= uni(o0)) return;
-  int start = 0, count = R;
+  const int B = map.bits[e];
+  int cls = 0, start = 0, count = R, rows = rows1 * stream_rt(B);
   if (routed) {
 #pragma unroll
     for (int c = 0; c < 4; c++) cnt[c] = uni(cnt[c]);
-    if (wgi < n_swg) {   // find the switched class of this workgroup
+    count = cnt[0];
+    if (sw) {   // find the switched class of this workgroup
+      rows = rows1;
       start = cnt[0];
       cls = 4;
       for (int c = 1; c < (NK == 1 ? 2 : 4); c++) {
@@ -479,13 +517,13 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split, int n_tt) {
         start += cnt[c];
       }
       if (cls == 4) return;
+      count = cnt[cls];
     }
-    count = cnt[cls];
   }
   const int pos0 = start + blk * rows;
   if (blk * rows >= count) return;
   const int pos1 = min(pos0 + rows, start + count);
-  const int B = map.bits[e - map.e0];
+  const int n_split = map.n_split;
   if constexpr (NT == 2) {
     // an expert with at most 16 tokens needs one 16-token tile: half the
     // contraction and epilogue work of the 32-token tile (same LDS)
@@ -514,16 +552,16 @@ ffn_stream_kernel(FfnArgs a, WgMap map, int n_split, int n_tt) {
 // once per group size (MOE_FFN_NM = 2 or 4, that is 64 or 128) to spread the
 // work over several compiler processes.
 #if !defined(MOE_FFN_NM) || MOE_FFN_NM == 2
-template __global__ void ffn_stream_kernel<2, 1, 1>(FfnArgs, WgMap, int, int);
-template __global__ void ffn_stream_kernel<2, 1, 2>(FfnArgs, WgMap, int, int);
-template __global__ void ffn_stream_kernel<2, 2, 1>(FfnArgs, WgMap, int, int);
-template __global__ void ffn_stream_kernel<2, 2, 2>(FfnArgs, WgMap, int, int);
+template __global__ void ffn_stream_kernel<2, 1, 1>(FfnArgs, WgMap);
+template __global__ void ffn_stream_kernel<2, 1, 2>(FfnArgs, WgMap);
+template __global__ void ffn_stream_kernel<2, 2, 1>(FfnArgs, WgMap);
+template __global__ void ffn_stream_kernel<2, 2, 2>(FfnArgs, WgMap);
 #endif
 #if !defined(MOE_FFN_NM) || MOE_FFN_NM == 4
-template __global__ void ffn_stream_kernel<4, 1, 1>(FfnArgs, WgMap, int, int);
-template __global__ void ffn_stream_kernel<4, 1, 2>(FfnArgs, WgMap, int, int);
-template __global__ void ffn_stream_kernel<4, 2, 1>(FfnArgs, WgMap, int, int);
-template __global__ void ffn_stream_kernel<4, 2, 2>(FfnArgs, WgMap, int, int);
+template __global__ void ffn_stream_kernel<4, 1, 1>(FfnArgs, WgMap);
+template __global__ void ffn_stream_kernel<4, 1, 2>(FfnArgs, WgMap);
+template __global__ void ffn_stream_kernel<4, 2, 1>(FfnArgs, WgMap);
+template __global__ void ffn_stream_kernel<4, 2, 2>(FfnArgs, WgMap);
 #endif
 
 }  // namespace ffn
