@@ -684,6 +684,58 @@ def measure_stress(hip, n_copies, steps=None):
                         "against the oracle in tests/test_gpu_stress.py"}
 
 
+def measure_unquantized(name, hip, steps, warmup=5, quantized_ms=None):
+    """The same step on the unquantized 16-bit reference layer: every expert
+    at bits = 16 (the bf16 values of the same seeded fp32 weights, no channel
+    copies, group 64) through the library's own kernels, on the quantized
+    workload's batch (same activations, same router bias).  The paper's only
+    performance figure is the speedup of the packed low-bit experts over a
+    16-bit model (Sec. VI-C); `speedup_of_quantized` is that ratio here."""
+    import torch
+    import moe_inputs as mi
+    import paper_2503_21135_amd as P
+    from paper_2503_21135_amd import api
+    wk = mi.WORKLOADS[name]
+    q_inputs = mi.LayerInputs(wk.layer)
+    inp = mi.LayerInputs(mi.unquantized(wk.layer))
+    lay = P.MoELayer(inp, device="cuda:0")
+    lay.set_epoch(0)
+    bt = mi.make_batch(wk, q_inputs)
+    x = torch.from_numpy(bt.x.view(np.int16)).to("cuda:0").view(torch.bfloat16)
+    bias = None if bt.bias is None else torch.from_numpy(bt.bias).to("cuda:0")
+    b = lay.buffers(wk.tokens)
+    for _ in range(warmup):
+        lay.forward(x, bias)
+    torch.cuda.synchronize()
+    ev = hip.create(2 * steps)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        lay.route(x, bias)
+        api.moe_expert_ffn_mixed_ev(lay.desc, x, lay.k, b.offsets, b.perm, b.o, b.ffn_ws,
+                                    (C.c_void_p * 5)(None, ev[2 * i], ev[2 * i + 1], None, None))
+        lay.combine(b)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    gu = float(np.mean([hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(steps)]))
+    hip.destroy(ev)
+    off = b.offsets.cpu().numpy()
+    byt = algorithmic_bytes(lay, off)
+    out = {"workload": "%s on the unquantized 16-bit layer (bf16 weights of the same fp32 draw, "
+                       "library kernels)" % name,
+           "ms_per_step": round(ms, 5), "tokens_per_s": round(wk.tokens / (ms * 1e-3), 1),
+           "gate_up_ms": round(gu, 5), "weight_bytes_per_step": int(byt["gate_up"] + byt["down"]),
+           "gate_up_gbs": round(byt["gate_up"] / (gu * 1e-3) / 1e9, 1),
+           "gate_up_tflops": round(flops_gate_up(lay, off) / (gu * 1e-3) / 1e12, 1)}
+    if quantized_ms:
+        out["speedup_of_quantized"] = round(ms / quantized_ms, 3)
+    del lay, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def measure_copy(mib=1024, reps=10):
     """GB/s of a plain device-to-device copy (bytes read + written), for context."""
     import torch
@@ -785,7 +837,8 @@ def main():
     ap.add_argument("--no-dataset-switch", action="store_true",
                     help="skip the timing of a requantization for a new dataset")
     ap.add_argument("--no-bf16", action="store_true",
-                    help="skip the unquantized bf16 reference of the same step")
+                    help="skip the unquantized 16-bit references of the same steps (the library's "
+                         "own kernels on bf16 weights, and torch's library GEMMs for context)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other workloads (DeepSeekMoE-shaped decode and prefill, "
                          "Qwen-shaped switch stress) that the default run also measures")
@@ -930,6 +983,14 @@ def main():
         extra["prefill"] = measure_prefill(layer, inputs, PREFILL_OF[args.workload], hip,
                                            args.prefill_steps, 5, bf16=not args.no_bf16)
         log("prefill", extra["prefill"])
+    if not args.no_bf16 and not wk.redraw_every:
+        # the unquantized 16-bit layer through the library's own kernels
+        u = {"decode": measure_unquantized(args.workload, hip, min(K, 50), 5, ms_per_step)}
+        if not args.no_prefill and args.workload in PREFILL_OF:
+            u["prefill"] = measure_unquantized(PREFILL_OF[args.workload], hip, args.prefill_steps, 3,
+                                               extra["prefill"]["ms_per_step"])
+        extra["unquantized_16bit"] = u
+        log("unquantized 16-bit", u)
     if not wk.redraw_every and not args.no_dataset_switch:
         # last: it rewrites the layer's copies
         extra["dataset_switch"] = measure_dataset_switch(layer, inputs, hip, ms_per_step)
@@ -948,6 +1009,15 @@ def main():
         log("deepseek prefill", extra["deepseek_prefill"])
         ds.clear()
         torch.cuda.empty_cache()
+        if not args.no_bf16:
+            extra["deepseek_unquantized_16bit"] = {
+                # against the cache-defeated (rotated) quantized step: the 16-bit layer
+                # (1.1 GB) does not fit the Infinity Cache either
+                "decode": measure_unquantized("deepseek-decode", hip, min(K, 50), 5,
+                                              extra["deepseek_decode"]["ms_per_step"]),
+                "prefill": measure_unquantized("deepseek-prefill", hip, args.prefill_steps, 3,
+                                               extra["deepseek_prefill"]["ms_per_step"])}
+            log("deepseek unquantized 16-bit", extra["deepseek_unquantized_16bit"])
         log("qwen-stress: %d copies, %d steps" % (n, mi.WORKLOADS["qwen-stress"].steps))
         extra["qwen_stress"] = measure_stress(hip, n)
         log("qwen stress", extra["qwen_stress"])

@@ -52,11 +52,12 @@ class LayerConfig:
     group: int
     bits_literal: Optional[Tuple[int, ...]] = None   # per routed expert
     bit_shares: Optional[Tuple[Tuple[int, float], ...]] = None
-    copies: str = "mask"        # 'all' | 'mask' | 'pool'
+    copies: str = "mask"        # 'all' | 'mask' | 'pool' | 'none'
     mask_frac: float = 0.05     # switched fraction ('all', 'mask')
     pool_frac: float = 0.10     # copy-pool fraction ('pool')
     outliers: int = 0           # input columns scaled x20
     weight_std: float = 0.02
+    shared_bits: int = 8        # bit-width of the shared experts
 
     def rows(self, kind: int, expert: int) -> int:
         f = self.d_ff if expert < self.n_experts else self.d_ff_shared
@@ -111,6 +112,18 @@ QWEN = LayerConfig(
     bit_shares=((8, 0.20), (4, 0.50), (3, 0.15), (2, 0.15)), copies="pool",
     pool_frac=0.10, outliers=20)
 
+def unquantized(cfg: LayerConfig) -> LayerConfig:
+    """The same layer (same seeded fp32 weights, router and activations)
+    with every expert, routed and shared, kept at 16 bits: the bf16 values of
+    the fp32 weights, no channel copies.  The reference for the speedup of
+    the packed low-bit weights over a 16-bit model (Sec. VI-C).  Group 64:
+    the library runs 16-bit experts in its group-64 kernels."""
+    import dataclasses
+    return dataclasses.replace(cfg, name=cfg.name + "-bf16", group=64, copies="none",
+                               bits_literal=(16,) * cfg.n_experts, bit_shares=None,
+                               shared_bits=16)
+
+
 WORKLOADS: Dict[str, Workload] = {
     "tiny": Workload("tiny", TINY, 16),
     "tiny-int6": Workload("tiny-int6", TINY6, 16),
@@ -162,7 +175,7 @@ class LayerInputs:
             routed = np.asarray(cfg.bits_literal, dtype=np.int32)
         else:
             routed = self._assign_bits(1)
-        self.bits = np.concatenate([routed, np.full(S, 8, np.int32)])
+        self.bits = np.concatenate([routed, np.full(S, cfg.shared_bits, np.int32)])
         self.router = (rng(seed, cfg.cfg_id, 0)
                        .standard_normal((E, cfg.d_model), dtype=np.float32)
                        * np.float32(cfg.weight_std))
@@ -227,7 +240,7 @@ class LayerInputs:
         """Copy headers (expert, row) of one kind, expert-major, rows ascending."""
         c = self.cfg
         hdr = []
-        for e in range(c.n_experts):
+        for e in range(c.n_experts if c.copies != "none" else 0):
             R = c.rows(kind, e)
             if c.copies == "all":
                 rows = np.arange(R, dtype=np.int32)
@@ -263,7 +276,7 @@ class LayerInputs:
         """Slots of the copy pool switched on in a mask epoch."""
         c = self.cfg
         hdr = self._pool[kind]
-        if c.copies == "mask":
+        if c.copies in ("mask", "none"):
             return np.arange(len(hdr), dtype=np.int32)
         if c.copies == "all":
             out = []
@@ -287,6 +300,8 @@ class LayerInputs:
         return np.concatenate(out).astype(np.int32)
 
     def switch_percent(self, epoch: int) -> int:
+        if self.cfg.copies == "none":
+            return 0
         if self.cfg.copies != "pool":
             return int(round(self.cfg.mask_frac * 100))
         return int(rng(self.seed, self.cfg.cfg_id, 3000 + epoch).integers(2, 11))

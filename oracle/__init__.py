@@ -67,6 +67,7 @@ def lib():
             "oracle_switch": (i32, [vp, i32, i32, i32, vp, i32, vp]),
             "oracle_expert_ffn": (None, [vp, vp, vp, i32, i32, vp, vp, i32, i32, vp]),
             "oracle_combine": (None, [vp, vp, vp, i32, i32, i32, i32, vp]),
+            "oracle_bf16_weights": (None, [vp, i64, vp]),
             "oracle_num_threads": (i32, []),
             "oracle_set_num_threads": (None, [i32]),
         }
@@ -286,6 +287,15 @@ def combine(o: np.ndarray, inv: np.ndarray, w: np.ndarray, k: int, S: int) -> np
     return y
 
 
+def bf16_weights(w: np.ndarray) -> np.ndarray:
+    """The unquantized 16-bit weights: each fp32 weight rounded to the nearest
+    bfloat16 (ties to even), as float64."""
+    w = np.ascontiguousarray(w, np.float32)
+    out = np.empty(w.shape, np.float64)
+    lib().oracle_bf16_weights(_ptr(w), w.size, _ptr(out))
+    return out
+
+
 def effective_weight(w_fp32: np.ndarray, bits: int, group: int,
                      switched_rows: Optional[np.ndarray] = None,
                      copy_bits: int = 0, copy_src16: Optional[np.ndarray] = None) -> np.ndarray:
@@ -294,7 +304,13 @@ def effective_weight(w_fp32: np.ndarray, bits: int, group: int,
     cache keeps the original channels).  With copy_bits == 0 the copy is the
     8-bit quantization of the original fp32 row; with copy_bits = b > 0 it is
     the b-bit requantization of the cached binary16 channel copy_src16[i] of
-    switched row i (requantization for a new dataset, Sec. IV-B)."""
+    switched row i (requantization for a new dataset, Sec. IV-B).  bits == 16
+    is the unquantized reference: the bf16 values of the fp32 weights (no
+    channel copies)."""
+    if bits == 16:
+        if switched_rows is not None and len(switched_rows):
+            raise ValueError("an unquantized expert has no channel copies")
+        return bf16_weights(w_fp32)
     st, q, s, z = quantize(w_fp32, bits, group)
     if st != OK:
         raise ValueError("oracle quantize: status %d" % st)
@@ -334,10 +350,7 @@ class LayerWeights:
         for e in (range(cfg.n_experts + cfg.n_shared) if experts is None else experts):
             for kind in (0, 1, 2):
                 w = layer.weight(e, kind)
-                st, q, s, z = quantize(w, int(layer.bits[e]), cfg.group)
-                if st != OK:
-                    raise ValueError("oracle quantize: status %d" % st)
-                self.base[(e, kind)] = dequant(q, s, z, cfg.group)
+                self.base[(e, kind)] = effective_weight(w, int(layer.bits[e]), cfg.group)
                 rows = np.unique(hdr[kind][hdr[kind][:, 0] == e, 1]) if e < cfg.n_experts else \
                     np.zeros(0, np.int64)
                 self.copy_rows[(e, kind)] = rows

@@ -125,6 +125,16 @@ uint16_t oracle_bf16_round(double v) {
   return (uint16_t)(u >> 16);
 }
 
+/*
+ * The unquantized 16-bit reference weights (the "FP16 model" the paper's
+ * speedup is measured against, Sec. VI-C, kept here in bfloat16 like the
+ * activations): each fp32 weight rounded to the nearest bfloat16, as binary64.
+ */
+void oracle_bf16_weights(const float* w, int64_t n, double* out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; i++) out[i] = oracle_bf16_value(oracle_bf16_round((double)w[i]));
+}
+
 /* ------------------------------------------------------------------------ */
 /* Quantization (Sec. IV-A: expert-level mixed precision, uniform quantizer)  */
 /* ------------------------------------------------------------------------ */

@@ -43,17 +43,21 @@ inline int launch_status(hipStream_t s) {
   return MOE_OK;
 }
 
+// Quantized bit-widths (codes, copies, requantization).
 inline bool valid_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
+// Widths an expert of the FFN may have: the quantized ones, or 16 for the
+// unquantized bf16 reference weights.
+inline bool valid_expert_bits(int b) { return valid_bits(b) || b == 16; }
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Row stride (32-bit words) of packed code matrices: K*bits/32 plus 64 bytes
-// (128 bytes at 8 bits), so that rows never start a power of two of bytes
+// (128 bytes at 8 and 16 bits), so that rows never start a power of two of bytes
 // apart -- a wavefront reads 16 rows at once, and rows 2^n bytes apart fall on
 // few HBM channels (measured on MI355X: 4-bit rows of 2048 bytes stream at
 // 6.1 TB/s unpadded, 6.8 TB/s padded).
 __host__ __device__ constexpr int64_t code_row_words(int64_t K, int bits) {
-  return K * bits / 32 + (bits == 8 ? 32 : 16);
+  return K * bits / 32 + (bits >= 8 ? 32 : 16);
 }
 
 // ---------------------------------------------------------------- device side

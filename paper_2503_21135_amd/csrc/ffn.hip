@@ -103,7 +103,8 @@ int validate_layer(const moe_layer_t* L) {
   if (fm * 4 * code_row_words(std::max<int64_t>(fm, L->d_model), 8) >= (int64_t{1} << 31))
     return MOE_ERR_ARG;
   for (int e = 0; e < E + S; e++) {
-    if (!valid_bits(L->bits_host[e])) return MOE_ERR_BITS;
+    if (!valid_expert_bits(L->bits_host[e])) return MOE_ERR_BITS;
+    if (L->bits_host[e] == 16 && L->group != 64) return MOE_ERR_ARG;   // unquantized experts: group 64
     if ((L->bits_host[e] == 3 || L->bits_host[e] == 6) && L->group != 128) return MOE_ERR_ARG;
   }
   for (int kd = 0; kd < 3; kd++) {
@@ -173,7 +174,7 @@ WgMap stream_map(const moe_layer_t* L, const Plan& p, bool routed, bool shared, 
   if (shared)
     for (int s = 0; s < S; s++) entry(E + s);
   if (routed)
-    for (int b : {8, 6, 4, 3, 2})
+    for (int b : {16, 8, 6, 4, 3, 2})
       for (int e = 0; e < E; e++)
         if (L->bits_host[e] == b) entry(e);
   m.ent_start[n] = start;

@@ -72,7 +72,7 @@ template <int B>
 constexpr int kPlanes = (B == 3 || B == 6) ? 2 : 1;
 
 template <int B>
-constexpr float kOffset = B == 8 ? 0.f : (B == 3 ? 640.f : (B == 6 ? 2176.f : 128.f));
+constexpr float kOffset = (B == 8 || B == 16) ? 0.f : (B == 3 ? 640.f : (B == 6 ? 2176.f : 128.f));
 
 // bf16 constant of the high plane of a two-plane width
 template <int BG, int BU>
@@ -112,6 +112,9 @@ __device__ __forceinline__ void dequant_b(const uint32_t (&cw)[NW], u32x4 (&wf)[
       wf[0][m] = u32x4{andor(w >> sh, 0x00030003u, vm), andor(w >> (sh + 2), 0x00030003u, vm),
                        andor(w >> (sh + 4), 0x00030003u, vm), andor(w >> (sh + 6), 0x00030003u, vm)};
     }
+  } else if constexpr (B == 16) {   // unquantized bf16 weights: the operand as stored
+#pragma unroll
+    for (int m = 0; m < NM; m++) wf[0][m] = u32x4{cw[4 * m], cw[4 * m + 1], cw[4 * m + 2], cw[4 * m + 3]};
   } else if constexpr (B == 8) {
 #pragma unroll
     for (int m = 0; m < NM; m++) {

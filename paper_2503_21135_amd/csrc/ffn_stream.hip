@@ -56,7 +56,7 @@ namespace ffn {
 // With two or four row tiles per wave (narrow codes) two groups in flight
 // already hold as many bytes as four groups of one row tile.
 template <int RT, int BG, int BU>
-constexpr int kStages = (RT >= 2 || BG == 8 || BU == 8 || BG == 6 || BU == 6) ? 2 : 4;
+constexpr int kStages = (RT >= 2 || BG >= 8 || BU >= 8 || BG == 6 || BU == 6) ? 2 : 4;
 
 
 // Metadata a workgroup loads in its prologue, all issued before any is
@@ -530,7 +530,9 @@ ffn_stream_kernel(FfnArgs a, WgMap map) {
     if (uni(o1) - uni(o0) <= 16) {
       auto& t1 = *reinterpret_cast<XTile<NM, 1>*>(&tl);
       if (B == 8) dispatch_class<NM, 1, NK, 8>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
-      else if (B == 4) dispatch_class<NM, 1, NK, 4>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      else if (NM == 2 && B == 16) {   // unquantized experts need group 64
+        if constexpr (NM == 2) dispatch_class<NM, 1, NK, 16>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
+      } else if (B == 4) dispatch_class<NM, 1, NK, 4>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
       else if (B == 2) dispatch_class<NM, 1, NK, 2>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
       else if constexpr (NM == 4) {
         if (B == 6) dispatch_class<NM, 1, NK, 6>(a, t1, pre, e, cls, pos0, pos1, R, sp, n_split);
@@ -540,7 +542,9 @@ ffn_stream_kernel(FfnArgs a, WgMap map) {
     }
   }
   if (B == 8) dispatch_class<NM, NT, NK, 8>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
-  else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  else if (NM == 2 && B == 16) {   // unquantized experts need group 64
+    if constexpr (NM == 2) dispatch_class<NM, NT, NK, 16>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
+  } else if (B == 4) dispatch_class<NM, NT, NK, 4>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
   else if (B == 2) dispatch_class<NM, NT, NK, 2>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);
   else if constexpr (NM == 4) {
     if (B == 6) dispatch_class<NM, NT, NK, 6>(a, tl, pre, e, cls, pos0, pos1, R, sp, n_split);

@@ -119,6 +119,17 @@ __device__ __forceinline__ uint32_t unpack16(uint32_t w, int sh, uint32_t m, uin
 template <int NM2, int B>
 __device__ __forceinline__ u32x4 dequant_h(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, f16x2 zneg, f16x2 sc,
                                            uint32_t vm) {
+  if constexpr (B == 16) {
+    // unquantized bf16 weights to fp16 (round toward zero: exact for every
+    // bf16 value in [2^-14, 65504], the fp16 normal range)
+    u32x4 out;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const uint32_t w = cw[4 * s + i];
+      out[i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(w), bf16_hi(w)));
+    }
+    return out;
+  }
   uint32_t r[4];
   if constexpr (B == 4) {
     const uint32_t w = cw[s];
@@ -475,7 +486,9 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
     const int B = map.bits[e - map.e0];
     if (B == 8) tile_dispatch<NM2, NK, 8>(a, tl, e, cls, pos0, pos1, R, t0, t1);
-    else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    else if (NM2 == 4 && B == 16) {   // unquantized experts need group 64
+      if constexpr (NM2 == 4) tile_dispatch<NM2, NK, 16>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
     else if (B == 2) tile_dispatch<NM2, NK, 2>(a, tl, e, cls, pos0, pos1, R, t0, t1);
     else if constexpr (NM2 % 4 == 0) {
       if (B == 6) tile_dispatch<NM2, NK, 6>(a, tl, e, cls, pos0, pos1, R, t0, t1);

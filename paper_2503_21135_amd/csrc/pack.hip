@@ -60,6 +60,13 @@ pack_kernel(const float* __restrict__ w, int64_t ld_w, int K, int bits, int grou
   const int r = rows ? rows[i] : i;
   const float* wg = w + static_cast<int64_t>(r) * ld_w + static_cast<int64_t>(j) * group;
 
+  if (bits == 16) {   // unquantized: the bf16 value of each weight, scale 1 and zero 0
+    uint32_t* out = codes + static_cast<int64_t>(i) * ld_codes + static_cast<int64_t>(j) * (group / 2);
+    for (int t = 0; t < group / 2; t++)
+      out[t] = bf16_rne(wg[2 * t]) | (bf16_rne(wg[2 * t + 1]) << 16);
+    sz[static_cast<int64_t>(i) * sz_rs + static_cast<int64_t>(j) * sz_gs] = 0x3C00u;
+    return;
+  }
   double mn = 0.0, mx = 0.0;
   for (int c = 0; c < group; c++) {
     const double v = static_cast<double>(wg[c]);
@@ -220,7 +227,7 @@ extern "C" int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K
                               int64_t sz_row_stride, int64_t sz_group_stride,
                               int32_t* status, void* stream) {
   using namespace moe;
-  if (!valid_bits(bits)) return MOE_ERR_BITS;
+  if (!valid_expert_bits(bits)) return MOE_ERR_BITS;
   if (!w || !codes || !sz || R <= 0 || K <= 0 || n < 0) return MOE_ERR_ARG;
   if (!(group == 64 || group == 128) || K % group || K % 32) return MOE_ERR_ARG;
   if ((bits == 3 || bits == 6) && group != 128) return MOE_ERR_ARG;
@@ -276,7 +283,7 @@ extern "C" const char* moe_status_str(int status) {
   switch (status) {
     case MOE_OK: return "ok";
     case MOE_ERR_ARG: return "invalid argument";
-    case MOE_ERR_BITS: return "bit-width not in {2,3,4,6,8}";
+    case MOE_ERR_BITS: return "bit-width not in {2,3,4,6,8} (or 16 where allowed)";
     case MOE_ERR_ALIGN: return "pointer or stride not 16-byte aligned";
     case MOE_ERR_WORKSPACE: return "workspace missing or too small";
     case MOE_ERR_SLOT: return "bad switch slot list";
@@ -287,6 +294,6 @@ extern "C" const char* moe_status_str(int status) {
 }
 
 extern "C" int64_t moe_code_row_words(int32_t K, int32_t bits) {
-  if (!moe::valid_bits(bits) || K <= 0 || K % 128) return 0;
+  if (!moe::valid_expert_bits(bits) || K <= 0 || K % 128) return 0;
   return moe::code_row_words(K, bits);
 }

@@ -68,6 +68,8 @@ def test_pack_validation(lib):
     assert call(codes=MISALIGNED) == -3
     assert call(ldc=33) == -3
     assert call(n=0) == 0           # nothing to do, no device call
+    assert call(b=16, ldc=127) == -1  # unquantized rows of K = 256 need 128 words
+    assert call(b=16, ldc=128, n=0) == 0
 
 
 def test_route_validation(lib):
@@ -171,6 +173,10 @@ def test_switch_and_ffn_validation(lib):
             break
         T *= 2
     assert na(C.byref(L), FAKE, T, 2, FAKE, FAKE, FAKE, None, None) == -4
+    b16 = np.array([8, 4, 16, 2], np.int32)   # an unquantized expert needs group 64
+    keep.append(b16)
+    L.bits_host = b16.ctypes.data
+    assert f(C.byref(L), FAKE, 16, 2, FAKE, FAKE, FAKE, FAKE, wb.value, None, None) == -1
     bits = np.array([8, 4, 5, 2], np.int32)
     keep.append(bits)
     L.bits_host = bits.ctypes.data
@@ -209,5 +215,6 @@ def test_code_row_words(lib):
     assert lib.moe_code_row_words(128, 2) == 8 + 16
     assert lib.moe_code_row_words(4096, 6) == 4096 * 6 // 32 + 16
     assert lib.moe_code_row_words(1408, 6) == 1408 * 6 // 32 + 16
-    for K, b in ((4096, 5), (100, 4), (0, 4), (-128, 8)):
+    assert lib.moe_code_row_words(4096, 16) == 4096 // 2 + 32   # unquantized bf16 rows
+    for K, b in ((4096, 5), (100, 4), (0, 4), (-128, 8), (4096, 12)):
         assert lib.moe_code_row_words(K, b) == 0

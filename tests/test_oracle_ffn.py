@@ -262,3 +262,26 @@ def test_layer_weights_cache_matches_fresh_quantization(orc):
     # a row without a cached copy cannot be switched
     with pytest.raises(ValueError):
         lw.effective(0, 0, np.array([wk.layer.d_ff + 5]))
+
+
+def test_bf16_reference_weights(orc):
+    # the unquantized 16-bit weights are the fp32 weights rounded to nearest
+    # bfloat16 with ties to even: torch's conversion, on random values and on
+    # hand-built ties (both directions) and magnitudes across the range
+    rng = np.random.default_rng(3)
+    w = (rng.standard_normal(50000) * 10.0 ** rng.uniform(-30, 30, 50000)).astype(np.float32)
+    ties = np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -(1.0 + 2.0 ** -8), 2.0 ** -130 * 1.5,
+                     0.0, -0.0, 3.4e38], np.float32)
+    w = np.concatenate([w, ties])
+    ref = torch.from_numpy(w).to(torch.bfloat16).double().numpy()
+    got = orc.bf16_weights(w)
+    assert np.array_equal(got, ref)
+    assert got[len(w) - 7] == 1.0 and got[len(w) - 6] == 1.0 + 2.0 ** -6   # ties to even
+    # an unquantized layer's effective weights are these values; no copies
+    cfg = mi.unquantized(mi.TINY)
+    inp = mi.LayerInputs(cfg)
+    assert list(inp.bits) == [16] * cfg.n_experts and len(inp.copy_headers(0)) == 0
+    W = orc.effective_weight(inp.weight(1, 0), 16, cfg.group)
+    assert np.array_equal(W, torch.from_numpy(inp.weight(1, 0)).to(torch.bfloat16).double().numpy())
+    with pytest.raises(ValueError):
+        orc.effective_weight(inp.weight(1, 0), 16, cfg.group, np.array([3]))
