@@ -317,7 +317,16 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     else if (ss) hs(a.Tk, a.rows);
   }
   if (p.nt_routed == 0) add_tile(down, one{}, false);
-  if (S > 0 && p.nt_shared == 0) add_tile(down, one{}, true);
+  if (S > 0 && p.nt_shared == 0) {
+    if (p.n_split > 1) {   // K splits exist only where routed rows stream: tiled shared rows need cleared slices
+      const int64_t off0 = static_cast<int64_t>(a.Tk) * a.d, n = static_cast<int64_t>(a.rows - a.Tk) * a.d;
+      const int64_t total = n * (p.n_split - 1);
+      down.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
+        klaunch(zero_slices_kernel, dim3(static_cast<unsigned>(cdiv(total, 256))), dim3(256), s, e0, e1, a, off0, n);
+      });
+    }
+    add_tile(down, one{}, true);
+  }
   add_stream(down, one{}, p.n_split);
   issue(xsum, event(0), nullptr, s);
   issue(gate_up, event(1), event(2), s);

@@ -37,7 +37,7 @@ struct FfnArgs {
   float* hsum;         // [max(f,fs)/g][rows] group sums of h rows
   float* o;
   int64_t split_stride;
-  int n_split_out;     // slices of o the combine adds (tile launches zero the others)
+  int n_split_out;     // slices of o the combine adds (zero_slices_kernel clears tiled rows)
   int32_t* tile_prefix;   // workspace: 4 x (MOE_MAX_EXPERTS + 1) item prefixes
   const uint16_t* x16;  // [T][d] fp16 copy of x (tile kernel; row of permuted row p: perm[p])
   int32_t* status;      // device status word or null: MOE_ERR_RANGE when an fp16 operand overflows
@@ -287,10 +287,10 @@ struct WgMap {
 
 constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token blocks)
 
-// Row positions per workgroup tile: eight waves of 32 rows, gate/up split
-// over the waves by kind (128 rows of both kinds) or down (256 rows).
+// Row positions per workgroup tile: eight waves, each with the gate and the
+// up row of 32 positions (256 positions) or 64 down rows (512 rows).
 template <int NK>
-constexpr int kTileRowsOf = NK == 2 ? 128 : 256;
+constexpr int kTileRowsOf = NK == 2 ? 256 : 512;
 
 constexpr int kTileWaves = 8;
 
@@ -316,6 +316,8 @@ group_sum_kernel(FfnArgs a, const uint16_t* __restrict__ in, const int32_t* __re
                  int64_t ld, int p0, int p1, int K, int p_split, int K2, float* __restrict__ out);
 
 __global__ void __launch_bounds__(256) gather_f16_kernel(FfnArgs a, int T);
+
+__global__ void __launch_bounds__(256) zero_slices_kernel(FfnArgs a, int64_t off0, int64_t n);
 
 template <int NK>
 __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, int32_t* __restrict__ prefix);

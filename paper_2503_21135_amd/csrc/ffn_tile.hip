@@ -20,17 +20,19 @@ namespace ffn {
 // exactly 1024 + q (q < 1024); one packed fp16 subtraction of 1024 + z makes
 // q - z exactly, one packed fp16 multiplication by s rounds the product.
 //
-// Eight waves per workgroup, two per SIMD.  Each wave owns 32 rows of one
-// kind (gate/up: waves 0-3 the gate rows, 4-7 the up rows of the tile's 128
-// positions; down: 256 rows) and all kTileTok tokens (four 32-token blocks),
-// so every dequantized B fragment feeds four MFMAs.  Lane l holds row l % 32
-// and the K-half l/32 of each group (group code g/2*half + 8*s + j feeds
-// K-step s, slot j); accumulator element r of lane l is token
+// Eight waves per workgroup, two per SIMD.  Each wave owns two weight rows
+// per lane column -- the gate and the up row of 32 positions (gate/up), or
+// two blocks of 32 positions 32 apart (down) -- and all kTileTok tokens
+// (four 32-token blocks): every activation fragment read from LDS feeds two
+// MFMAs and every dequantized weight fragment four.  Lane l holds position
+// l % 32 and the K-half l/32 of each group (group code g/2*half + 8*s + j
+// feeds K-step s, slot j); accumulator element r of lane l is token
 // 8*(r/4) + 4*(l/32) + r%4 of the block.  The activations of one group for
-// the whole tile are staged in LDS by direct-to-LDS loads, two groups ahead
-// (three stages), with the XOR swizzle of the streaming kernel; the packed
-// codes of the next three groups are in flight in registers.  The SiLU-GLU
-// epilogue meets the gate and up sums of a row through LDS.
+// the whole tile are staged in LDS by direct-to-LDS loads, NS-1 groups ahead,
+// with the XOR swizzle of the streaming kernel; the packed codes of the next
+// NS groups are in flight in registers (NS = 3 stages, or 2 where the codes of
+// a group take many registers).  Gate/up applies SiLU-GLU to its own two
+// accumulators.
 //
 // Work items (expert, row block, token tile) come from a prefix table a small
 // plan kernel builds from the routing offsets and class counts, and are
@@ -51,20 +53,26 @@ __device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const 
 
 constexpr uint32_t kMagic16 = 0x64006400u;   // two fp16 1024.0
 
-// LDS of the tile kernel: three stages of kTileTok token rows x g columns of
-// fp16 activations in 16-byte slots (slot s: token s / (g/8), column chunk
+// One LDS stage of the tile kernel: kTileTok token rows x g columns of fp16
+// activations in 16-byte slots (slot s: token s / (g/8), column chunk
 // (s % (g/8)) ^ (token % (g/8))).
 template <int NM2>
-struct HTile {
+struct TileStage {
   static constexpr int g = NM2 * 16;
   static constexpr int SPT = g / 8;
   static constexpr int SLOTS = kTileTok * SPT;
-  union {
-    u32x4 a[3][SLOTS];
-    float xch[4 * 4 * 16 * 64];   // gate/up epilogue: the up sums of four 32-row blocks
-  };
 };
 
+// The stages are three separate __shared__ arrays: the compiler then knows
+// that the direct-to-LDS loads into one stage do not write what the waves
+// read from another, and waits for none of them before its reads.
+struct TileLds {
+  u32x4* s0;
+  u32x4* s1;
+  u32x4* s2;
+};
+
+__device__ __forceinline__ u32x4* stage_of(const TileLds& l, int b) { return b == 0 ? l.s0 : (b == 1 ? l.s1 : l.s2); }
 
 // Items of expert e: (row blocks over its classes) x (token tiles); the
 // exclusive prefix over the launch's experts goes to prefix[0 .. n_e].
@@ -188,17 +196,30 @@ struct HCodes {
   uint32_t szw;
 };
 
+// Vector-memory instructions of one row's group in hload: the code loads and,
+// except for unquantized weights (whose {s, z} word the dequantization does
+// not read), the {s, z} load.  The waits of the tile kernel count these
+// exactly: a load the compiler could drop as unused must not be issued.
+template <int NM2, int BW>
+constexpr int kGroupLoads = kCodeLoads<(kHalfWords<NM2, BW>)> + (BW == 16 ? 0 : 1);
+
 template <int NM2, int BW>
 __device__ __forceinline__ void hload(HCodes<NM2, BW>& st, const TSrc& sr, int gi, bool gv) {
   constexpr uint32_t gcb = NM2 * 16 * BW / 8;   // code bytes per row and group
   bload<kHalfWords<NM2, BW>>(st.cw, sr.code, gv ? sr.coff : kOOB, gv ? gi * gcb : 0u);
-  st.szw = __builtin_amdgcn_raw_buffer_load_b32(sr.sz, gv ? sr.soff : kOOB, gv ? gi * sr.sz_gstride : 0u, 0);
+  if constexpr (BW == 16) st.szw = 0u;
+  else st.szw = __builtin_amdgcn_raw_buffer_load_b32(sr.sz, gv ? sr.soff : kOOB, gv ? gi * sr.sz_gstride : 0u, 0);
 }
 
-template <int N>
+// Wait until at most N vector-memory instructions are in flight.  Loads
+// complete in issue order, so this makes every load issued before the last N
+// complete.  The comment names the stage count and whether the wait ends the
+// prologue, for the check of these counts against the compiled code
+// (tests/test_tile_waits.py).
+template <int N, int NS, int PRO>
 __device__ __forceinline__ void hwait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt field");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+  asm volatile("s_waitcnt vmcnt(%0) ; tile-wait ns=%1 pro=%2" ::"n"(N), "n"(NS), "n"(PRO) : "memory");
 }
 
 // Barrier without __syncthreads()' fences (those would drain the in-flight
@@ -211,59 +232,81 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
   return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
 }
 
-// Activation stages in flight: the stage of group gi+2 is loaded while group
-// gi is contracted; three LDS stages.
-constexpr int kAStages = 3;
+// Stages of a tile item: 3 (codes of three groups and activations of two
+// groups in flight) where the two sources' codes of a group take at most 16
+// registers, else 2 (the accumulators of both sources leave no room).
+template <int NM2, int BW0, int BW1>
+constexpr int kTileStages = ((kHalfWords<NM2, BW0>) + (kHalfWords<NM2, BW1>) <= 16) ? 3 : 2;
 
-// One wave's share of a tile item: 32 rows (position block rb) of weight kind
-// kk, whose source has width BW (the expert's base width, or 8 for the
-// cached copies of a switched class), against all kTileTok tokens.
-template <int NM2, int NK, int BW, int TB>
-__device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int e, bool copy, int be, int kk,
-                                          int rb, int pos0, int pos1, int R, int t0, int t1) {
+// Buffer source of one weight row of kind `kind`: the expert's own codes of
+// width be, or the cached 8-bit copy of the row (copy).
+template <int NM2>
+__device__ __forceinline__ TSrc tile_src(const FfnArgs& a, int kind, bool copy, int be, int e, int R, int K, int row,
+                                         bool live, int kh) {
   constexpr int g = NM2 * 16;
-  constexpr int SPT = HTile<NM2>::SPT;
+  const int G = K / g;
+  const KindDev& kd = a.kd[kind];
+  const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
+  const uint32_t crow_bytes = 4u * static_cast<uint32_t>(code_row_words(K, 8));
+  const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
+                          : static_cast<const void*>(kd.codes + uni(kd.code_off[e]));
+  const void* sptr = copy ? static_cast<const void*>(kd.copy_sz)
+                          : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
+  const uint32_t cbytes = copy ? a.copy_bytes[kind] : static_cast<uint32_t>(R) * row_bytes;
+  const uint32_t sbytes = copy ? a.copy_sz_bytes[kind] : static_cast<uint32_t>(R) * G * 4u;
+  TSrc src;
+  src.code = make_rsrc(cptr, cbytes);
+  src.sz = make_rsrc(sptr, sbytes);
+  src.sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
+  const int slot = (copy && live) ? kd.row_slot[static_cast<int64_t>(e) * R + row] : -1;
+  const uint32_t c_base = live ? row * row_bytes + kh * (g / 2) * be / 8 : kOOB;
+  const uint32_t s_base = live ? row * 4u : kOOB;
+  const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * crow_bytes + kh * (g / 2) : kOOB;
+  const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
+  src.coff = copy ? c_copy : c_base;
+  src.soff = copy ? s_copy : s_base;
+  return src;
+}
+
+// One wave's share of a tile item against all of the item's tokens (TB
+// 32-token blocks): gate/up takes the gate row (source 0) and the up row
+// (source 1) of the positions 32*wave .. +31 of the item; down takes two
+// blocks of 32 positions, 64*wave and 64*wave + 32.  Source j has width BWj
+// (the expert's base width be, or 8 where it reads the cached copies of a
+// switched class, copyj).
+template <int NM2, int NK, int BW0, int BW1, int TB>
+__device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, int e, bool copy0, bool copy1, int be,
+                                          int pos0, int pos1, int R, int t0, int t1) {
+  constexpr int g = NM2 * 16;
+  constexpr int SPT = TileStage<NM2>::SPT;
   // activation slots of the tile's TB token blocks, and loads per thread and
   // stage (slots past them are written with zeros)
   constexpr int SL = TB * 32 * SPT;
   constexpr int NLD = (SL + 64 * kTileWaves - 1) / (64 * kTileWaves);
   constexpr bool down = NK == 1;
-  // vector-memory instructions of one group's code and {s, z} loads
-  constexpr int LC = kCodeLoads<(kHalfWords<NM2, BW>)> + 1;
+  constexpr int NS = kTileStages<NM2, BW0, BW1>;
+  // vector-memory instructions of one group's code and {s, z} loads (both
+  // sources), and the loads that may stay in flight once the codes and the
+  // activation stage of the next group have landed
+  constexpr int LCG = kGroupLoads<NM2, BW0> + kGroupLoads<NM2, BW1>;
+  constexpr int WAITN = NS == 3 ? 2 * LCG + NLD : LCG;
   const int tid = threadIdx.x;
-  const int wv = tid >> 6, lane = tid & 63;
+  const int wv = uni(static_cast<int>(tid >> 6));
+  const int lane = tid & 63;
   const int n = lane & 31, kh = lane >> 5;
   const bool routed = e < a.E;
   const int K = down ? (routed ? a.f : a.fs) : a.d;
   const int G = K / g;
-  const int kind0 = down ? 2 : 0;
   const int32_t* order = down ? a.order_dn : a.order_gu;
-  const int pos = pos0 + 32 * rb + n;
-  const bool live = pos < pos1;
-  const int row = live ? (routed ? order[static_cast<int64_t>(e) * R + pos] : pos) : 0;
+  const int wpos = pos0 + (down ? 64 : 32) * wv;
+  const bool wlive = wpos < pos1;   // wave-uniform: a wave past the class's end only stages and waits
+  const int q0 = wpos + n, q1 = down ? q0 + 32 : q0;
+  const bool live0 = q0 < pos1, live1 = q1 < pos1;
+  const int row0 = live0 ? (routed ? order[static_cast<int64_t>(e) * R + q0] : q0) : 0;
+  const int row1 = down ? (live1 ? (routed ? order[static_cast<int64_t>(e) * R + q1] : q1) : 0) : row0;
+  const TSrc src0 = tile_src<NM2>(a, down ? 2 : 0, copy0, be, e, R, K, row0, live0, kh);
+  const TSrc src1 = tile_src<NM2>(a, down ? 2 : 1, copy1, be, e, R, K, row1, live1, kh);
 
-  TSrc src;
-  {
-    const KindDev& kd = a.kd[kind0 + kk];
-    const uint32_t row_bytes = 4u * static_cast<uint32_t>(code_row_words(K, be));
-    const uint32_t crow_bytes = 4u * static_cast<uint32_t>(code_row_words(K, 8));
-    const void* cptr = copy ? static_cast<const void*>(kd.copy_codes)
-                            : static_cast<const void*>(kd.codes + uni(kd.code_off[e]));
-    const void* sptr = copy ? static_cast<const void*>(kd.copy_sz)
-                            : static_cast<const void*>(kd.sz + uni(kd.sz_off[e]));
-    const uint32_t cbytes = copy ? a.copy_bytes[kind0 + kk] : static_cast<uint32_t>(R) * row_bytes;
-    const uint32_t sbytes = copy ? a.copy_sz_bytes[kind0 + kk] : static_cast<uint32_t>(R) * G * 4u;
-    src.code = make_rsrc(cptr, cbytes);
-    src.sz = make_rsrc(sptr, sbytes);
-    src.sz_gstride = copy ? 4u : static_cast<uint32_t>(R) * 4u;
-    const int slot = (copy && live) ? kd.row_slot[static_cast<int64_t>(e) * R + row] : -1;
-    const uint32_t c_base = live ? row * row_bytes + kh * (g / 2) * be / 8 : kOOB;
-    const uint32_t s_base = live ? row * 4u : kOOB;
-    const uint32_t c_copy = slot >= 0 ? static_cast<uint32_t>(slot) * crow_bytes + kh * (g / 2) : kOOB;
-    const uint32_t s_copy = slot >= 0 ? static_cast<uint32_t>(slot) * G * 4u : kOOB;
-    src.coff = copy ? c_copy : c_base;
-    src.soff = copy ? s_copy : s_base;
-  }
   // fp16 activations: gathered x rows (gate/up) or h rows (down), row p of the
   // permuted order; slot i of this thread's loads
   const Rsrc xr = make_rsrc(down ? static_cast<const void*>(a.h) : static_cast<const void*>(a.x16),
@@ -282,150 +325,152 @@ __device__ __forceinline__ void tile_wave(const FfnArgs& a, HTile<NM2>& tl, int 
   auto stage_a = [&](int buf, int gi) {
     const bool gv = gi < G;
     const uint32_t adv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
+    u32x4* st = stage_of(lds, buf);
 #pragma unroll
-    for (int i = 0; i < NLD; i++)
-      lds_dma16(xr, &tl.a[buf][64 * kTileWaves * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
+    for (int i = 0; i < NLD; i++) lds_dma16(xr, &st[64 * kTileWaves * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
   };
 
   // the OR operand of the unpacking in a vector register (one v_and_or_b32)
   uint32_t vm = kMagic16;
   asm volatile("" : "+v"(vm));
-  f32x16 acc[TB];
+  f32x16 acc0[TB], acc1[TB];
 #pragma unroll
-  for (int tb = 0; tb < TB; tb++) acc[tb] = f32x16{};
+  for (int tb = 0; tb < TB; tb++) {
+    acc0[tb] = f32x16{};
+    acc1[tb] = f32x16{};
+  }
 
-  HCodes<NM2, BW> cs[3];
+  HCodes<NM2, BW0> c0[NS];
+  HCodes<NM2, BW1> c1[NS];
+  auto load = [&](HCodes<NM2, BW0>& x0, HCodes<NM2, BW1>& x1, int gi) {
+    hload<NM2, BW0>(x0, src0, gi, gi < G);
+    hload<NM2, BW1>(x1, src1, gi, gi < G);
+  };
   stage_a(0, 0);
-  hload<NM2, BW>(cs[0], src, 0, 0 < G);
-  stage_a(1, 1);
-  hload<NM2, BW>(cs[1], src, 1, 1 < G);
-  hload<NM2, BW>(cs[2], src, 2, 2 < G);
-  hwait_vm<2 * LC + NLD>();   // activations of group 0 have landed (this wave's share)
-  tile_barrier();             // ... every wave's share
+  load(c0[0], c1[0], 0);
+  if constexpr (NS == 3) stage_a(1, 1);
+  load(c0[1], c1[1], 1);
+  if constexpr (NS == 3) load(c0[2], c1[2], 2);
+  hwait_vm<WAITN, NS, 1>();   // codes and activations of group 0 have landed (this wave's share)
+  tile_barrier();      // ... every wave's share
 
-  auto group = [&](HCodes<NM2, BW>& c, int buf, int gi) {
-    stage_a((buf + 2) % kAStages, gi + 2);   // that stage was last read for group gi-1 (barrier since)
-    if (gi < G) {   // workgroup-uniform (G is odd for some shapes)
-      f16x2 zn, sc;
-      sz_pair(c.szw, zn, sc);
+  auto group = [&](HCodes<NM2, BW0>& x0, HCodes<NM2, BW1>& x1, int buf, int gi) {
+    // that stage was last read for group gi-1 (barrier since)
+    stage_a((buf + NS - 1) % NS, gi + NS - 1);
+    if (gi < G && wlive) {   // workgroup-uniform G (odd for some shapes), wave-uniform wlive
+      const u32x4* st = stage_of(lds, buf);
+      // the slot of K-step s and token block tb is a0 ^ s plus 32*SPT*tb
+      // (n % SPT is the swizzle of every token block, and s < NM2 touches
+      // only the low bits of kh*NM2); a0 passes through an empty asm so the
+      // eight K-step addresses are formed here, not kept live over the loop
+      uint32_t a0 = static_cast<uint32_t>(n * SPT + ((kh * NM2) ^ (n % SPT)));
+      asm volatile("" : "+v"(a0));
+      f16x2 zn0, sc0, zn1, sc1;
+      sz_pair(x0.szw, zn0, sc0);
+      sz_pair(x1.szw, zn1, sc1);
 #pragma unroll
       for (int s = 0; s < NM2; s++) {
         u32x4 af[TB];
+        const uint32_t as = a0 ^ static_cast<uint32_t>(s);
 #pragma unroll
-        for (int tb = 0; tb < TB; tb++) {
-          const int t = tb * 32 + n;
-          af[tb] = tl.a[buf][t * SPT + ((kh * NM2 + s) ^ (t % SPT))];
-        }
-        const u32x4 bf = dequant_h<NM2, BW>(c.cw, s, zn, sc, vm);
+        for (int tb = 0; tb < TB; tb++) af[tb] = st[as + 32 * SPT * tb];
+        const u32x4 b0 = dequant_h<NM2, BW0>(x0.cw, s, zn0, sc0, vm);
+        const u32x4 b1 = dequant_h<NM2, BW1>(x1.cw, s, zn1, sc1, vm);
 #pragma unroll
-        for (int tb = 0; tb < TB; tb++) acc[tb] = mfma32h(af[tb], bf, acc[tb]);
+        for (int tb = 0; tb < TB; tb++) acc0[tb] = mfma32h(af[tb], b0, acc0[tb]);
+#pragma unroll
+        for (int tb = 0; tb < TB; tb++) acc1[tb] = mfma32h(af[tb], b1, acc1[tb]);
       }
     }
-    hload<NM2, BW>(c, src, gi + 3, gi + 3 < G);
-    hwait_vm<2 * LC + NLD>();   // everything but the last two code loads and the newest stage: group gi+1's
+    load(x0, x1, gi + NS);
+    hwait_vm<WAITN, NS, 0>();   // everything but the newer loads: group gi+1's codes and activations
     tile_barrier();
   };
-  for (int gi = 0; gi < G; gi += 3) {
-    group(cs[0], 0, gi);
-    group(cs[1], 1, gi + 1);
-    group(cs[2], 2, gi + 2);
+  for (int gi = 0; gi < G; gi += NS) {
+    group(c0[0], c1[0], 0, gi);
+    group(c0[1], c1[1], 1, gi + 1);
+    if constexpr (NS == 3) group(c0[2], c1[2], 2, gi + 2);
   }
-  hwait_vm<0>();
+  hwait_vm<0, 0, 0>();
+  if (!wlive) return;
 
-  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4, row `row`
-  if constexpr (NK == 2) {
-    // the up waves hand their sums to the gate waves of the same rows through
-    // the (now idle) activation stages; same lane layout on both sides
-    float* xch = tl.xch;
-    tile_barrier();   // every wave is done reading the activation stages
-    if (kk == 1) {
-#pragma unroll
-      for (int tb = 0; tb < TB; tb++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) xch[((rb * 4 + tb) * 16 + r) * 64 + lane] = acc[tb][r];
-    }
-    tile_barrier();
-    if (kk == 0) {
-      // rows of one item are all routed or all shared: one h row width
-      const int hw = t0 < a.Tk ? a.f : a.fs;
-      uint16_t* hbase = a.h + h_row(a, t0 + 4 * kh) + row;
-      bool bad = false;
-#pragma unroll
-      for (int tb = 0; tb < TB; tb++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-          const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
-          const float u = xch[((rb * 4 + tb) * 16 + r) * 64 + lane];
-          if (live && t0 + 4 * kh + dt < t1) {
-            // h = bf16(silu(g) * u), stored as its fp16 value (exact unless
-            // it is below 2^-17 in magnitude or beyond fp16's range)
-            const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc[tb][r], u)) << 16);
-            hbase[dt * hw] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
-            bad = bad || !fp16_finite(hb);
-          }
-        }
-      if (bad && a.status) *a.status = MOE_ERR_RANGE;
-    }
-  } else {
-    float* obase = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row;
+  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4
+  if constexpr (!down) {
+    // rows of one item are all routed or all shared: one h row width
+    const int hw = t0 < a.Tk ? a.f : a.fs;
+    uint16_t* hbase = a.h + h_row(a, t0 + 4 * kh) + row0;
+    bool bad = false;
 #pragma unroll
     for (int tb = 0; tb < TB; tb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
-        if (live && t0 + 4 * kh + dt < t1) obase[dt * R] = acc[tb][r];
-      }
-    // the other split slices of these rows (the combine adds every slice)
-    for (int sp = 1; sp < a.n_split_out; sp++) {
-      float* ob = obase + static_cast<int64_t>(sp) * a.split_stride;
-#pragma unroll
-      for (int tb = 0; tb < TB; tb++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-          const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
-          if (live && t0 + 4 * kh + dt < t1) ob[dt * R] = 0.f;
+        if (live0 && t0 + 4 * kh + dt < t1) {
+          // h = bf16(silu(g) * u), stored as its fp16 value (exact unless
+          // it is below 2^-17 in magnitude or beyond fp16's range)
+          const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc0[tb][r], acc1[tb][r])) << 16);
+          hbase[dt * hw] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
+          bad = bad || !fp16_finite(hb);
         }
-    }
-  }
-}
-
-// Waves 0-3 take the gate rows and waves 4-7 the up rows of the tile's 128
-// positions, or all eight waves take 32 of the 256 down rows; a kind whose
-// class bit is set reads the 8-bit copies.
-template <int NM2, int NK, int B>
-__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, HTile<NM2>& tl, int e, int cls, int pos0,
-                                              int pos1, int R, int t0, int t1) {
-  // the wave index through readfirstlane: the kind, the class bit and the
-  // buffer descriptors chosen by them are then scalar values, so no load is
-  // wrapped in a loop over the distinct descriptors of the wave's lanes
-  const int wv = uni(static_cast<int>(threadIdx.x >> 6));
-  const int kk = NK == 2 ? wv / 4 : 0;
-  const int rb = NK == 2 ? wv % 4 : wv;
-  const bool copy = (cls >> kk) & 1;
-  // the expert's base width: class 1 or 2 has one kind on copies, whose
-  // template width is 8 even though the base width is B.  The token tile of
-  // the item (an expert's last tile is partial) picks one, two or four
-  // 32-token blocks.
-  const int nt = t1 - t0;
-  if (nt <= 32) {
-    if (copy) tile_wave<NM2, NK, 8, 1>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
-    else tile_wave<NM2, NK, B, 1>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
-  } else if (nt <= 64) {
-    if (copy) tile_wave<NM2, NK, 8, 2>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
-    else tile_wave<NM2, NK, B, 2>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+      }
+    if (bad && a.status) *a.status = MOE_ERR_RANGE;
   } else {
-    if (copy) tile_wave<NM2, NK, 8, 4>(a, tl, e, true, B, kk, rb, pos0, pos1, R, t0, t1);
-    else tile_wave<NM2, NK, B, 4>(a, tl, e, false, B, kk, rb, pos0, pos1, R, t0, t1);
+    // slice 0 of o; the host clears the other split slices of tiled rows
+    float* ob0 = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row0;
+    float* ob1 = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row1;
+#pragma unroll
+    for (int tb = 0; tb < TB; tb++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) {
+        const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
+        if (t0 + 4 * kh + dt < t1) {
+          if (live0) ob0[dt * R] = acc0[tb][r];
+          if (live1) ob1[dt * R] = acc1[tb][r];
+        }
+      }
   }
 }
 
-// Eight waves, two per SIMD: a wave's 64 accumulator registers leave room for
-// a second wave, which hides the first one's load and LDS latencies.
+// The class of an item picks each source's width: gate/up class bit j set =
+// kind j reads the 8-bit copies; down class 1 = copies.  The token tile of
+// the item (an expert's last tile is partial) picks one, two or four 32-token
+// blocks.
+template <int NM2, int NK, int B>
+__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, const TileLds& lds, int e, int cls, int pos0,
+                                              int pos1, int R, int t0, int t1) {
+  const int nt = t1 - t0;
+  auto by_tb = [&](auto w0, auto w1, bool c0, bool c1) {
+    constexpr int W0 = decltype(w0)::value, W1 = decltype(w1)::value;
+    if (nt <= 32) tile_item<NM2, NK, W0, W1, 1>(a, lds, e, c0, c1, B, pos0, pos1, R, t0, t1);
+    else if (nt <= 64) tile_item<NM2, NK, W0, W1, 2>(a, lds, e, c0, c1, B, pos0, pos1, R, t0, t1);
+    else tile_item<NM2, NK, W0, W1, 4>(a, lds, e, c0, c1, B, pos0, pos1, R, t0, t1);
+  };
+  using WB = std::integral_constant<int, B>;
+  using W8 = std::integral_constant<int, 8>;
+  if constexpr (NK == 1) {
+    if (cls & 1) by_tb(W8{}, W8{}, true, true);
+    else by_tb(WB{}, WB{}, false, false);
+  } else if constexpr (B == 8) {
+    by_tb(W8{}, W8{}, (cls & 1) != 0, (cls & 2) != 0);
+  } else {
+    if (cls == 0) by_tb(WB{}, WB{}, false, false);
+    else if (cls == 1) by_tb(W8{}, WB{}, true, false);
+    else if (cls == 2) by_tb(WB{}, W8{}, false, true);
+    else by_tb(W8{}, W8{}, true, true);
+  }
+}
+
+// Eight waves, two per SIMD: a wave's accumulators (two sources x four token
+// blocks, 128 registers) leave room for a second wave, which hides the
+// first one's load and LDS latencies.
 template <int NM2, int NK>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
 ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
-  __shared__ __attribute__((aligned(16))) HTile<NM2> tl;
+  __shared__ __attribute__((aligned(16))) u32x4 st0[TileStage<NM2>::SLOTS];
+  __shared__ __attribute__((aligned(16))) u32x4 st1[TileStage<NM2>::SLOTS];
+  __shared__ __attribute__((aligned(16))) u32x4 st2[TileStage<NM2>::SLOTS];
   __shared__ int pre[MOE_MAX_EXPERTS + 1];
+  const TileLds lds{st0, st1, st2};
   for (int i = threadIdx.x; i <= map.n_e; i += blockDim.x) pre[i] = prefix[i];
   __syncthreads();
   const int total = pre[map.n_e];
@@ -485,14 +530,14 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     const int pos1 = min(pos0 + kTileRowsOf<NK>, start + count);
     const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
     const int B = map.bits[e - map.e0];
-    if (B == 8) tile_dispatch<NM2, NK, 8>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+    if (B == 8) tile_dispatch<NM2, NK, 8>(a, lds, e, cls, pos0, pos1, R, t0, t1);
     else if (NM2 == 4 && B == 16) {   // unquantized experts need group 64
-      if constexpr (NM2 == 4) tile_dispatch<NM2, NK, 16>(a, tl, e, cls, pos0, pos1, R, t0, t1);
-    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, tl, e, cls, pos0, pos1, R, t0, t1);
-    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+      if constexpr (NM2 == 4) tile_dispatch<NM2, NK, 16>(a, lds, e, cls, pos0, pos1, R, t0, t1);
+    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, lds, e, cls, pos0, pos1, R, t0, t1);
+    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, lds, e, cls, pos0, pos1, R, t0, t1);
     else if constexpr (NM2 % 4 == 0) {
-      if (B == 6) tile_dispatch<NM2, NK, 6>(a, tl, e, cls, pos0, pos1, R, t0, t1);
-      else tile_dispatch<NM2, NK, 3>(a, tl, e, cls, pos0, pos1, R, t0, t1);
+      if (B == 6) tile_dispatch<NM2, NK, 6>(a, lds, e, cls, pos0, pos1, R, t0, t1);
+      else tile_dispatch<NM2, NK, 3>(a, lds, e, cls, pos0, pos1, R, t0, t1);
     }
     tile_barrier();   // the LDS stages are reused by the next item
   }
