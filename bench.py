@@ -29,6 +29,25 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 
 
+def reap_children():
+    """Nothing this run started may outlive it: the oracle's build (gcc) and
+    the library's build run as waited-for subprocesses and the thread pools
+    are joined, so no child is expected; any that is left is named on stderr
+    and ended."""
+    try:
+        import psutil
+    except ImportError:
+        return
+    kids = psutil.Process().children(recursive=True)
+    for c in kids:
+        try:
+            log("ending child process %d (%s)" % (c.pid, " ".join(c.cmdline()[:4])))
+            c.terminate()
+        except psutil.Error:
+            pass
+    psutil.wait_procs(kids, timeout=5)
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -1076,6 +1095,7 @@ def main():
         },
     }
     print(json.dumps(out), flush=True)
+    reap_children()
 
 
 if __name__ == "__main__":
