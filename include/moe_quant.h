@@ -55,6 +55,10 @@
  * 16+i).  For b = 6 every block of 32 codes takes six words: words 0..3 hold
  * bits 0..3 of codes 8w..8w+7 (word w) in the 4-bit half-split order, words
  * 4 and 5 bits 4..5 of codes 0..15 and 16..31 in the 2-bit half-split order.
+ * b = 16 is the unquantized reference layout (the 16-bit model that the
+ * paper's speedups are measured against, Sec. VI-C): word i holds the bf16
+ * values (round to nearest even) of weights 2i (low half) and 2i+1 (high
+ * half), and every {scale, zero} word is {1.0, 0}.
  * Quantization groups run along K: group j covers codes
  * [j*group, (j+1)*group) of a row.
  *
@@ -87,6 +91,11 @@
  *     (absolute error <= 2^-25); beyond 65504 (and for inf or NaN) it has no
  *     finite fp16 value, and the call reports it through its status word
  *     (MOE_ERR_RANGE) instead of silently producing infinities.
+ * Unquantized experts (bits 16) take the same two routes: the streaming
+ * kernel multiplies their bf16 weights as stored; the tile kernel converts
+ * them to fp16 rounding toward zero, exact for magnitudes in [2^-17, 65504]
+ * (smaller ones truncate to the fp16 subnormal grid, absolute error < 2^-24;
+ * larger ones clamp to +-65504).
  * Either way the FFN output matches the exact definition to within 2e-3
  * relative L2 (measured: ~1e-4 for the first, ~1.1e-3 for the second).
  */
@@ -103,7 +112,7 @@ extern "C" {
 /* Status codes. */
 #define MOE_OK             0
 #define MOE_ERR_ARG       -1  /* bad size, NULL pointer or inconsistent arguments      */
-#define MOE_ERR_BITS      -2  /* bit-width outside {2, 3, 4, 6, 8}                      */
+#define MOE_ERR_BITS      -2  /* bit-width outside {2, 3, 4, 6, 8} (or 16 where allowed) */
 #define MOE_ERR_ALIGN     -3  /* a pointer that must be 16-byte aligned is not          */
 #define MOE_ERR_WORKSPACE -4  /* workspace NULL or smaller than the size helper returns */
 #define MOE_ERR_SLOT      -5  /* switch slot out of range, duplicated, or two slots
@@ -125,10 +134,10 @@ extern "C" {
 /*
  * moe_code_row_words -- row stride, in 32-bit words, of the packed code
  * matrices moe_expert_ffn_mixed reads (base codes and 8-bit copies): K*bits/32
- * words of codes followed by padding of 16 words (32 words at bits == 8), so
+ * words of codes followed by padding of 16 words (32 words at bits >= 8), so
  * that consecutive rows never start a power of two of bytes apart.  The
- * padding words are never read.  Returns 0 for bits outside {2, 3, 4, 6, 8} or
- * K not a positive multiple of 128.
+ * padding words are never read.  Returns 0 for bits outside {2, 3, 4, 6, 8, 16}
+ * or K not a positive multiple of 128.
  */
 int64_t moe_code_row_words(int32_t K, int32_t bits);
 
@@ -173,7 +182,8 @@ typedef struct moe_kind_desc {
 /*
  * One MoE layer.  Routed experts have hidden size d_ff, shared experts
  * d_ff_shared (shared experts are always applied with weight 1 and are never
- * switched).  bits[e] in {2, 3, 4, 6, 8}; bit-widths 3 and 6 need group == 128.
+ * switched).  bits[e] in {2, 3, 4, 6, 8}, or 16 for an unquantized expert
+ * (bf16 weights); bit-widths 3 and 6 need group == 128, 16 needs group == 64.
  *
  * order_gu[e*d_ff + i] and order_dn[e*d_model + i] (routed experts only) are
  * the orders in which the FFN visits hidden neurons and output channels.  They
@@ -208,7 +218,8 @@ typedef struct moe_layer {
  *   w        device fp32 [R][ld_w]; the rows to quantize are rows[0..n-1]
  *            (device int32 list) or, when rows == NULL, rows 0..n-1 (n <= R).
  *   K        codes per row; K % group == 0, K % 32 == 0.
- *   bits     2, 3, 4, 6 or 8.  group   64 or 128 (3- and 6-bit need 128).
+ *   bits     2, 3, 4, 6 or 8, or 16 (the bf16 values, {1.0, 0} words).
+ *   group    64 or 128 (3- and 6-bit need 128).
  *   codes    device; list row i is written to codes[i*ld_codes ...], K*bits/32
  *            words; ld_codes >= K*bits/32; codes and ld_codes*4 16-byte aligned.
  *   sz       device; {s16, z} word of (list row i, group j) is written to

@@ -128,8 +128,9 @@ template <int NM2, int B>
 __device__ __forceinline__ u32x4 dequant_h(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, f16x2 zneg, f16x2 sc,
                                            uint32_t vm) {
   if constexpr (B == 16) {
-    // unquantized bf16 weights to fp16 (round toward zero: exact for every
-    // bf16 value in [2^-14, 65504], the fp16 normal range)
+    // unquantized bf16 weights to fp16, rounding toward zero: exact for every
+    // bf16 magnitude in [2^-17, 65504] (its last significand bit is >= 2^-24,
+    // the fp16 subnormal spacing); larger magnitudes clamp to 65504
     u32x4 out;
 #pragma unroll
     for (int i = 0; i < 4; i++) {
