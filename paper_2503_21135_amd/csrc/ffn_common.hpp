@@ -287,10 +287,10 @@ struct WgMap {
 
 constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token blocks)
 
-// Row positions per workgroup tile: eight waves, each with the gate and the
-// up row of 32 positions (256 positions) or 64 down rows (512 rows).
+// Row positions per wave of the tile kernel: the gate and the up row of 32
+// positions, or 64 down rows.  A workgroup's item is eight such waves.
 template <int NK>
-constexpr int kTileRowsOf = NK == 2 ? 256 : 512;
+constexpr int kTileWaveRows = NK == 2 ? 32 : 64;
 
 constexpr int kTileWaves = 8;
 

@@ -8,7 +8,7 @@ namespace ffn {
 // ------------------------------------------------------------------ tile kernel
 // For experts with many tokens (prefill, shared experts), where the
 // contraction is MFMA-bound: a workgroup computes a tile of kTileTok tokens x
-// kTileRowsOf<NK> row positions with v_mfma_f32_32x32x16_f16.  This is
+// eight waves' row positions with v_mfma_f32_32x32x16_f16.  This is
 // the paper's formulation of the dequantized product (Sec. V-B: dequantize to
 // a 16-bit operand, then matrix-core multiply): the weight operand is
 // fp16(s * (q - z)) -- one rounding per weight -- and the activations enter
@@ -34,8 +34,13 @@ namespace ffn {
 // a group take many registers).  Gate/up applies SiLU-GLU to its own two
 // accumulators.
 //
-// Work items (expert, row block, token tile) come from a prefix table a small
-// plan kernel builds from the routing offsets and class counts, and are
+// An expert's row positions are cut into waves class by class (each source
+// class of the row order -- base codes, or copies for the gate, the up or both
+// rows -- starts a new wave), and eight consecutive waves form a row block;
+// a wave's class picks its sources, so a small class costs one wave, not a
+// workgroup.  Work items (expert, row block, token tile) come from a prefix
+// table a small plan kernel builds from the routing offsets and class
+// counts, and are
 // spread over a persistent grid so that the workgroups of one XCD (hardware
 // places workgroup b on XCD b % 8) take consecutive items.  Within an expert
 // the items run in super-tiles of kSuper row blocks x kSuper token tiles, so
@@ -74,7 +79,36 @@ struct TileLds {
 
 __device__ __forceinline__ u32x4* stage_of(const TileLds& l, int b) { return b == 0 ? l.s0 : (b == 1 ? l.s1 : l.s2); }
 
-// Items of expert e: (row blocks over its classes) x (token tiles); the
+// Waves of expert e: class c of its row order (routed experts; a shared
+// expert is one class of R rows) takes ceil(count / kTileWaveRows) waves,
+// classes in order.  pre[c] = first wave of class c (pre[NC] = the total),
+// beg[c] / cnt[c] = its positions.  UNI: e is the same in every lane (the
+// counts then go through readfirstlane, so they are scalar values).
+template <int NK>
+struct TileWaves {
+  static constexpr int NC = NK == 1 ? 2 : 4;
+  int pre[NC + 1], beg[NC], cnt[NC];
+};
+
+template <int NK, bool UNI>
+__device__ __forceinline__ TileWaves<NK> tile_waves(const FfnArgs& a, int e, int R) {
+  constexpr int NC = TileWaves<NK>::NC;
+  TileWaves<NK> w;
+  w.pre[0] = 0;
+  int start = 0;
+#pragma unroll
+  for (int c = 0; c < NC; c++) {
+    int cn = e < a.E ? a.class_cnt[(NK == 1 ? 4 * a.E : 0) + 4 * e + c] : (c == 0 ? R : 0);
+    if constexpr (UNI) cn = uni(cn);
+    w.beg[c] = start;
+    w.cnt[c] = cn;
+    w.pre[c + 1] = w.pre[c] + (cn + kTileWaveRows<NK> - 1) / kTileWaveRows<NK>;
+    start += cn;
+  }
+  return w;
+}
+
+// Items of expert e: (row blocks of eight waves) x (token tiles); the
 // exclusive prefix over the launch's experts goes to prefix[0 .. n_e].
 template <int NK>
 __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, int32_t* __restrict__ prefix) {
@@ -85,14 +119,9 @@ __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, 
     const int e = map.e0 + i;
     const int n_tok = a.offsets[e + 1] - a.offsets[e];
     const int tiles = (n_tok + kTileTok - 1) / kTileTok;
-    int blocks = 0;
-    if (e < a.E) {
-      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
-      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) blocks += (cc[c] + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
-    } else {
-      blocks = ((NK == 1 ? a.d : a.fs) + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
-    }
-    items = tiles * blocks;
+    const int R = NK == 1 ? a.d : (e < a.E ? a.f : a.fs);
+    const TileWaves<NK> w = tile_waves<NK, false>(a, e, R);
+    items = tiles * ((w.pre[TileWaves<NK>::NC] + kTileWaves - 1) / kTileWaves);
   }
   if (i < MOE_MAX_EXPERTS) cnt[i] = items;
   __syncthreads();
@@ -270,14 +299,16 @@ __device__ __forceinline__ TSrc tile_src(const FfnArgs& a, int kind, bool copy, 
 }
 
 // One wave's share of a tile item against all of the item's tokens (TB
-// 32-token blocks): gate/up takes the gate row (source 0) and the up row
-// (source 1) of the positions 32*wave .. +31 of the item; down takes two
-// blocks of 32 positions, 64*wave and 64*wave + 32.  Source j has width BWj
-// (the expert's base width be, or 8 where it reads the cached copies of a
-// switched class, copyj).
-template <int NM2, int NK, int BW0, int BW1, int TB>
+// 32-token blocks), over its positions [wpos, wend) of the expert's row
+// order (one class; wpos >= wend for a wave past the expert's last class):
+// gate/up takes the gate row (source 0) and the up row (source 1) of 32
+// positions; down takes two blocks of 32 positions, wpos and wpos + 32.
+// Source j has width BWj (the expert's base width be, or 8 where it reads the
+// cached copies of a switched class, copyj).  NS, the item's stage count, is
+// the same in every wave of the workgroup.
+template <int NM2, int NK, int NS, int BW0, int BW1, int TB>
 __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, int e, bool copy0, bool copy1, int be,
-                                          int pos0, int pos1, int R, int t0, int t1) {
+                                          int wpos, int wend, int R, int t0, int t1) {
   constexpr int g = NM2 * 16;
   constexpr int SPT = TileStage<NM2>::SPT;
   // activation slots of the tile's TB token blocks, and loads per thread and
@@ -285,7 +316,7 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
   constexpr int SL = TB * 32 * SPT;
   constexpr int NLD = (SL + 64 * kTileWaves - 1) / (64 * kTileWaves);
   constexpr bool down = NK == 1;
-  constexpr int NS = kTileStages<NM2, BW0, BW1>;
+  static_assert(NS == 2 || (NS == 3 && kTileStages<NM2, BW0, BW1> == 3), "register budget of the code stages");
   // vector-memory instructions of one group's code and {s, z} loads (both
   // sources), and the loads that may stay in flight once the codes and the
   // activation stage of the next group have landed
@@ -299,10 +330,9 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
   const int K = down ? (routed ? a.f : a.fs) : a.d;
   const int G = K / g;
   const int32_t* order = down ? a.order_dn : a.order_gu;
-  const int wpos = pos0 + (down ? 64 : 32) * wv;
-  const bool wlive = wpos < pos1;   // wave-uniform: a wave past the class's end only stages and waits
+  const bool wlive = wpos < wend;   // wave-uniform: a wave without positions only stages and waits
   const int q0 = wpos + n, q1 = down ? q0 + 32 : q0;
-  const bool live0 = q0 < pos1, live1 = q1 < pos1;
+  const bool live0 = q0 < wend, live1 = q1 < wend;
   const int row0 = live0 ? (routed ? order[static_cast<int64_t>(e) * R + q0] : q0) : 0;
   const int row1 = down ? (live1 ? (routed ? order[static_cast<int64_t>(e) * R + q1] : q1) : 0) : row0;
   const TSrc src0 = tile_src<NM2>(a, down ? 2 : 0, copy0, be, e, R, K, row0, live0, kh);
@@ -432,32 +462,34 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
   }
 }
 
-// The class of an item picks each source's width: gate/up class bit j set =
-// kind j reads the 8-bit copies; down class 1 = copies.  The token tile of
-// the item (an expert's last tile is partial) picks one, two or four 32-token
-// blocks.
+// The wave's class picks each source's width: gate/up class bit j set =
+// kind j reads the 8-bit copies; down class 1 = copies.  The item's stage
+// count: the narrow widths' three stages where every wave of the item is of
+// class 0, else two.  The token tile of the item (an expert's last tile is
+// partial) picks one, two or four 32-token blocks.
 template <int NM2, int NK, int B>
-__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, const TileLds& lds, int e, int cls, int pos0,
-                                              int pos1, int R, int t0, int t1) {
+__device__ __forceinline__ void tile_dispatch(const FfnArgs& a, const TileLds& lds, int e, int cls, bool base_item,
+                                              int wpos, int wend, int R, int t0, int t1) {
   const int nt = t1 - t0;
-  auto by_tb = [&](auto w0, auto w1, bool c0, bool c1) {
-    constexpr int W0 = decltype(w0)::value, W1 = decltype(w1)::value;
-    if (nt <= 32) tile_item<NM2, NK, W0, W1, 1>(a, lds, e, c0, c1, B, pos0, pos1, R, t0, t1);
-    else if (nt <= 64) tile_item<NM2, NK, W0, W1, 2>(a, lds, e, c0, c1, B, pos0, pos1, R, t0, t1);
-    else tile_item<NM2, NK, W0, W1, 4>(a, lds, e, c0, c1, B, pos0, pos1, R, t0, t1);
+  auto by_tb = [&](auto ns, auto w0, auto w1, bool c0, bool c1) {
+    constexpr int NS = decltype(ns)::value, W0 = decltype(w0)::value, W1 = decltype(w1)::value;
+    if (nt <= 32) tile_item<NM2, NK, NS, W0, W1, 1>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1);
+    else if (nt <= 64) tile_item<NM2, NK, NS, W0, W1, 2>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1);
+    else tile_item<NM2, NK, NS, W0, W1, 4>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1);
   };
   using WB = std::integral_constant<int, B>;
   using W8 = std::integral_constant<int, 8>;
-  if constexpr (NK == 1) {
-    if (cls & 1) by_tb(W8{}, W8{}, true, true);
-    else by_tb(WB{}, WB{}, false, false);
-  } else if constexpr (B == 8) {
-    by_tb(W8{}, W8{}, (cls & 1) != 0, (cls & 2) != 0);
+  using S2 = std::integral_constant<int, 2>;
+  using SB = std::integral_constant<int, kTileStages<NM2, B, B>>;
+  if (cls == 0) {
+    if (base_item) by_tb(SB{}, WB{}, WB{}, false, false);
+    else by_tb(S2{}, WB{}, WB{}, false, false);
+  } else if constexpr (NK == 1 || B == 8) {
+    by_tb(S2{}, W8{}, W8{}, (cls & 1) != 0, NK == 1 || (cls & 2) != 0);
   } else {
-    if (cls == 0) by_tb(WB{}, WB{}, false, false);
-    else if (cls == 1) by_tb(W8{}, WB{}, true, false);
-    else if (cls == 2) by_tb(WB{}, W8{}, false, true);
-    else by_tb(W8{}, W8{}, true, true);
+    if (cls == 1) by_tb(S2{}, W8{}, WB{}, true, false);
+    else if (cls == 2) by_tb(S2{}, WB{}, W8{}, false, true);
+    else by_tb(S2{}, W8{}, W8{}, true, true);
   }
 }
 
@@ -492,15 +524,13 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     const int tiles = (seg1 - seg0 + kTileTok - 1) / kTileTok;
     const bool routed = e < a.E;
     const int R = NK == 1 ? a.d : (routed ? a.f : a.fs);
+    // the expert's waves, class after class; eight waves per row block
+    const TileWaves<NK> w = tile_waves<NK, true>(a, e, R);
+    constexpr int NC = TileWaves<NK>::NC;
+    const int n_w = w.pre[NC];
+    const int n_rb = (n_w + kTileWaves - 1) / kTileWaves;
     // (row block, token tile) of the local index: super-rows of kSuper row
     // blocks, token tiles outer and row blocks inner within a super-row
-    int n_rb = 0;
-    if (routed) {
-      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
-      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) n_rb += (uni(cc[c]) + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
-    } else {
-      n_rb = (R + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
-    }
     const int full = (n_rb / kSuper) * kSuper * tiles;
     int rb, tt;
     if (local < full) {
@@ -512,33 +542,27 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
       tt = rem / h;
       rb = (n_rb / kSuper) * kSuper + rem % h;
     }
-    int cls = 0, start = 0, count = R;
-    if (routed) {
-      const int32_t* cc = a.class_cnt + (NK == 1 ? 4 * a.E : 0) + 4 * e;
-      for (int c = 0; c < (NK == 1 ? 2 : 4); c++) {
-        const int cn = uni(cc[c]);
-        const int nb = (cn + kTileRowsOf<NK> - 1) / kTileRowsOf<NK>;
-        if (rb < nb) {
-          cls = c;
-          count = cn;
-          break;
-        }
-        rb -= nb;
-        start += cn;
-      }
-    }
-    const int pos0 = start + rb * kTileRowsOf<NK>;
-    const int pos1 = min(pos0 + kTileRowsOf<NK>, start + count);
+    // this wave's class and positions; the item runs three stages only when
+    // all of its waves are of class 0
+    const int gw = rb * kTileWaves + uni(static_cast<int>(threadIdx.x >> 6));
+    int cls = 0;
+#pragma unroll
+    for (int c = 1; c < NC; c++) cls += gw >= w.pre[c] ? 1 : 0;
+    const bool dead = gw >= n_w;
+    const int wpos = dead ? 0 : w.beg[cls] + (gw - w.pre[cls]) * kTileWaveRows<NK>;
+    const int wend = dead ? 0 : min(wpos + kTileWaveRows<NK>, w.beg[cls] + w.cnt[cls]);
+    if (dead) cls = 0;
+    const bool base_item = min((rb + 1) * kTileWaves, n_w) <= w.pre[1];
     const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
     const int B = map.bits[e - map.e0];
-    if (B == 8) tile_dispatch<NM2, NK, 8>(a, lds, e, cls, pos0, pos1, R, t0, t1);
+    if (B == 8) tile_dispatch<NM2, NK, 8>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
     else if (NM2 == 4 && B == 16) {   // unquantized experts need group 64
-      if constexpr (NM2 == 4) tile_dispatch<NM2, NK, 16>(a, lds, e, cls, pos0, pos1, R, t0, t1);
-    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, lds, e, cls, pos0, pos1, R, t0, t1);
-    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, lds, e, cls, pos0, pos1, R, t0, t1);
+      if constexpr (NM2 == 4) tile_dispatch<NM2, NK, 16>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
+    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
+    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
     else if constexpr (NM2 % 4 == 0) {
-      if (B == 6) tile_dispatch<NM2, NK, 6>(a, lds, e, cls, pos0, pos1, R, t0, t1);
-      else tile_dispatch<NM2, NK, 3>(a, lds, e, cls, pos0, pos1, R, t0, t1);
+      if (B == 6) tile_dispatch<NM2, NK, 6>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
+      else tile_dispatch<NM2, NK, 3>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
     }
     tile_barrier();   // the LDS stages are reused by the next item
   }
