@@ -290,6 +290,39 @@ def test_tile_sets_with_split_k(orc):
     assert err <= TOL and err <= DIAG_STREAM
 
 
+def test_shared_tile_beside_split_k(orc):
+    # 16 routed experts at ~75 tokens stream over 32-token tile sets with the
+    # down projection split over K, while the shared expert sees all 600
+    # tokens and goes to the tile kernel: the tile kernel writes slice 0 of
+    # its rows and the other slice of those rows must be zero for the
+    # combine's sum
+    import dataclasses
+    import paper_2503_21135_amd as P
+    from paper_2503_21135_amd import api
+    bits = (8, 4, 6, 2, 3, 4, 8, 2, 4, 6, 4, 3, 2, 8, 4, 4)
+    cfg = dataclasses.replace(mi.TINY6, name="shared-tile-splitk", cfg_id=8, n_experts=16, n_shared=1,
+                              d_ff=2048, d_ff_shared=2048, bits_literal=bits)
+    inp = mi.LayerInputs(cfg)
+    layer = P.MoELayer(inp)
+    T = 600
+    n_split, _ = api.moe_ffn_plan(layer.desc, T, cfg.top_k)
+    assert n_split == 2
+    layer.set_epoch(0)
+    rs = oracle_row_slots(orc, inp)
+    x = mi.make_x(cfg, T, stream=970)
+    # garbage in every slice first: the zeros must come from this call
+    b = layer.buffers(T)
+    b.o.fill_(123.0)
+    y, b = _run(layer, x)
+    Tk = T * cfg.top_k
+    assert torch.count_nonzero(b.o[1, Tk:]).item() == 0
+    res = orc.layer_forward(inp, x, row_slot=rs)
+    routing_matches(layer, res, b)
+    err = rel_l2(y, res["y"])
+    print("shared tile + split-K", "rel_l2", err, flush=True)
+    assert err <= TOL and err <= DIAG_TILE
+
+
 def test_fp16_operand_range_status(orc):
     # The tile kernel (prefill sizes) multiplies fp16 copies of the
     # activations and of h: a value with no finite fp16 value is reported
