@@ -161,11 +161,15 @@ def measured_traffic(workload):
 
 
 def ffn_source_hash():
-    """Hash of the expert-FFN kernel sources (the counters are valid for them only)."""
+    """Hash of the expert-FFN kernel sources without their comments and
+    layout (the counters are valid for that code only)."""
     h = hashlib.sha256()
     for f in FFN_SOURCES:
-        with open(os.path.join(ROOT, "paper_2503_21135_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2503_21135_amd", "csrc", f)) as fh:
+            src = fh.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 

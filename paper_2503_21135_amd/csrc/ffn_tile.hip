@@ -13,7 +13,8 @@ namespace ffn {
 // a 16-bit operand, then matrix-core multiply): the weight operand is
 // fp16(s * (q - z)) -- one rounding per weight -- and the activations enter
 // as fp16 (the bf16 activations and hidden values convert exactly while
-// their magnitude stays below 65504).  The scale is thus inside the operand
+// their magnitude lies in [2^-17, 65504]; a value beyond 65504 sets the
+// call's status word to MOE_ERR_RANGE).  The scale is thus inside the operand
 // and the accumulation runs over the whole K with no per-group epilogue.
 //
 // Dequantization: a code q OR-ed into the mantissa of fp16 1024.0 gives
@@ -31,8 +32,8 @@ namespace ffn {
 // the whole tile are staged in LDS by direct-to-LDS loads, NS-1 groups ahead,
 // with the XOR swizzle of the streaming kernel; the packed codes of the next
 // NS groups are in flight in registers (NS = 3 stages, or 2 where the codes of
-// a group take many registers).  Gate/up applies SiLU-GLU to its own two
-// accumulators.
+// a group take many registers or the item mixes source classes).  Gate/up
+// applies SiLU-GLU to its own two accumulators.
 //
 // An expert's row positions are cut into waves class by class (each source
 // class of the row order -- base codes, or copies for the gate, the up or both
@@ -40,9 +41,8 @@ namespace ffn {
 // a wave's class picks its sources, so a small class costs one wave, not a
 // workgroup.  Work items (expert, row block, token tile) come from a prefix
 // table a small plan kernel builds from the routing offsets and class
-// counts, and are
-// spread over a persistent grid so that the workgroups of one XCD (hardware
-// places workgroup b on XCD b % 8) take consecutive items.  Within an expert
+// counts, and are spread over a persistent grid so that the workgroups of one
+// XCD (hardware places workgroup b on XCD b % 8) take consecutive items.  Within an expert
 // the items run in super-tiles of kSuper row blocks x kSuper token tiles, so
 // that the workgroups one XCD runs together share both their code rows and
 // their activation rows through that XCD's L2.
