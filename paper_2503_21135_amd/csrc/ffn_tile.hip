@@ -57,6 +57,7 @@ __device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const 
 }
 
 constexpr uint32_t kMagic16 = 0x64006400u;   // two fp16 1024.0
+constexpr uint32_t kHigh64 = 0x64646464u;    // the high byte of fp16 1024.0, in every byte
 
 // One LDS stage of the tile kernel: kTileTok token rows x g columns of fp16
 // activations in 16-byte slots (slot s: token s / (g/8), column chunk
@@ -152,63 +153,42 @@ __device__ __forceinline__ uint32_t unpack16(uint32_t w, int sh, uint32_t m, uin
   return ((w >> sh) & m) | vm;
 }
 
-// B fragment of K-step s: 8 fp16 weights s*(q - z) of this lane's row.
+// Component i (weights 2i, 2i+1) of the B fragment of K-step s: two fp16
+// weights s*(q - z) of this lane's row.
 template <int NM2, int B>
-__device__ __forceinline__ u32x4 dequant_h(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, f16x2 zneg, f16x2 sc,
-                                           uint32_t vm) {
+__device__ __forceinline__ uint32_t dequant_h1(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, int i, f16x2 zneg,
+                                               f16x2 sc, uint32_t vm) {
   if constexpr (B == 16) {
     // unquantized bf16 weights to fp16, rounding toward zero: exact for every
     // bf16 magnitude in [2^-17, 65504] (its last significand bit is >= 2^-24,
     // the fp16 subnormal spacing); larger magnitudes clamp to 65504
-    u32x4 out;
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const uint32_t w = cw[4 * s + i];
-      out[i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(w), bf16_hi(w)));
-    }
-    return out;
+    const uint32_t w = cw[4 * s + i];
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(w), bf16_hi(w)));
   }
-  uint32_t r[4];
+  uint32_t r;
   if constexpr (B == 4) {
-    const uint32_t w = cw[s];
-#pragma unroll
-    for (int i = 0; i < 4; i++) r[i] = unpack16(w, 4 * i, 0x000F000Fu, vm);
+    r = unpack16(cw[s], 4 * i, 0x000F000Fu, vm);
   } else if constexpr (B == 8) {
-    const uint32_t w0 = cw[2 * s], w1 = cw[2 * s + 1];   // bytes (c0, c2, c1, c3)
-    r[0] = unpack16(w0, 0, 0x00FF00FFu, vm);
-    r[1] = unpack16(w0, 8, 0x00FF00FFu, vm);
-    r[2] = unpack16(w1, 0, 0x00FF00FFu, vm);
-    r[3] = unpack16(w1, 8, 0x00FF00FFu, vm);
+    // bytes (c0, c2, c1, c3): one byte permute with 0x64 bytes per pair gives
+    // (0x64 << 8 | q) = 1024 + q in both halves
+    r = __builtin_amdgcn_perm(kHigh64, cw[2 * s + (i >> 1)], (i & 1) ? 0x04030401u : 0x04020400u);
   } else if constexpr (B == 2) {
-    const uint32_t w = cw[s >> 1];
-    const int o = (s & 1) * 8;
-#pragma unroll
-    for (int i = 0; i < 4; i++) r[i] = unpack16(w, o + 2 * i, 0x00030003u, vm);
+    r = unpack16(cw[s >> 1], (s & 1) * 8 + 2 * i, 0x00030003u, vm);
   } else if constexpr (B == 6) {  // per 32-code block: words 0-3 bits 0..3, words 4-5 bits 4..5
     const int blk = 6 * (s >> 2);
     const int q = s & 3;   // octet within the block
     const uint32_t lo = cw[blk + q], hi = cw[blk + 4 + (q >> 1)];
     const int o = (q & 1) * 8;
-#pragma unroll
-    for (int i = 0; i < 4; i++)
-      r[i] = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | vm;
+    r = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | vm;
   } else {  // 3-bit: per 32-code block words (low plane 0-15, low plane 16-31, high plane)
     const int blk = 3 * (s >> 2);
     const int q = s & 3;   // octet within the block
     const uint32_t lo = cw[blk + (q >> 1)], hi = cw[blk + 2];
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int pi = 4 * q + i;   // pair index within the block
-      r[i] = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | vm;
-    }
+    const int pi = 4 * q + i;   // pair index within the block
+    r = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | vm;
   }
-  u32x4 out;
-#pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const f16x2 d = __builtin_bit_cast(f16x2, r[i]) + zneg;   // q - z, exact
-    out[i] = __builtin_bit_cast(uint32_t, d * sc);            // s * (q - z), rounded once
-  }
-  return out;
+  const f16x2 d = __builtin_bit_cast(f16x2, r) + zneg;   // q - z, exact
+  return __builtin_bit_cast(uint32_t, d * sc);            // s * (q - z), rounded once
 }
 
 // {s, z} word -> packed (-(1024 + z), -(1024 + z)) and (s, s).
@@ -399,18 +379,37 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
       f16x2 zn0, sc0, zn1, sc1;
       sz_pair(x0.szw, zn0, sc0);
       sz_pair(x1.szw, zn1, sc1);
+      // Software pipeline over the K-steps, fixed by scheduling fences (the
+      // compiler would otherwise move each LDS read next to its first MFMA
+      // and wait for it there): each MFMA of source 0 is issued with a
+      // quarter of source 1's fragment; each MFMA of source 1 with the next
+      // K-step's read into the activation register it has just read last
+      // and a quarter of source 0's next fragment.
+      u32x4 af[TB], b0, b1;
+#pragma unroll
+      for (int tb = 0; tb < TB; tb++) af[tb] = st[a0 + 32 * SPT * tb];
+#pragma unroll
+      for (int i = 0; i < 4; i++) b0[i] = dequant_h1<NM2, BW0>(x0.cw, 0, i, zn0, sc0, vm);
 #pragma unroll
       for (int s = 0; s < NM2; s++) {
-        u32x4 af[TB];
-        const uint32_t as = a0 ^ static_cast<uint32_t>(s);
+        const uint32_t an = a0 ^ static_cast<uint32_t>(s + 1);
 #pragma unroll
-        for (int tb = 0; tb < TB; tb++) af[tb] = st[as + 32 * SPT * tb];
-        const u32x4 b0 = dequant_h<NM2, BW0>(x0.cw, s, zn0, sc0, vm);
-        const u32x4 b1 = dequant_h<NM2, BW1>(x1.cw, s, zn1, sc1, vm);
+        for (int tb = 0; tb < TB; tb++) {
+          acc0[tb] = mfma32h(af[tb], b0, acc0[tb]);
 #pragma unroll
-        for (int tb = 0; tb < TB; tb++) acc0[tb] = mfma32h(af[tb], b0, acc0[tb]);
+          for (int i = tb; i < 4; i += TB) b1[i] = dequant_h1<NM2, BW1>(x1.cw, s, i, zn1, sc1, vm);
+          __builtin_amdgcn_sched_barrier(0);
+        }
 #pragma unroll
-        for (int tb = 0; tb < TB; tb++) acc1[tb] = mfma32h(af[tb], b1, acc1[tb]);
+        for (int tb = 0; tb < TB; tb++) {
+          acc1[tb] = mfma32h(af[tb], b1, acc1[tb]);
+          if (s + 1 < NM2) {
+            af[tb] = st[an + 32 * SPT * tb];
+#pragma unroll
+            for (int i = tb; i < 4; i += TB) b0[i] = dequant_h1<NM2, BW0>(x0.cw, s + 1, i, zn0, sc0, vm);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
     load(x0, x1, gi + NS);
