@@ -33,6 +33,27 @@ constexpr int kSharedSplitMax = 512;
 // workgroup sets taking every n_tt-th 32-token tile of the expert.
 constexpr int kRoutedSplitMax = 96;
 
+// Persistent tile grid: one workgroup of eight waves per compute unit (two
+// waves per SIMD), a multiple of the XCD count.
+int tile_grid() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
+    cached[dev] = std::max(kXcds, cu / kXcds * kXcds);
+  }
+  return cached[dev];
+}
+
+// Split-K of the tile kernel's down projection: slices (at most
+// kTileSplitMax, each at least kTileSplitMinGroups groups of K) until the
+// estimated items reach kTileItemsPerWg per workgroup of the grid.
+constexpr int kTileSplitMax = 4;
+constexpr int kTileItemsPerWg = 4;
+constexpr int kTileSplitMinGroups = 8;
+
 // Streaming kernel for up to 28 expected tokens per expert (one or two
 // 16-token MFMA tiles, weights streamed once); beyond, make_plan spreads the
 // 32-token tiles of mid-sized experts over workgroup sets, and the rest go to
@@ -72,9 +93,23 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
     p.nt_shared = 2;
     p.tt_shared = static_cast<int>(cdiv(T, 32));
   }
-  // split-K slices of the down projection only where the routed experts
-  // stream (few tokens, too few output rows to fill the machine)
-  p.n_split = p.nt_routed == 0 ? 1 : std::max(ns, 1);
+  // split-K slices of the down projection: where the routed experts stream
+  // (few tokens, too few output rows to fill the machine), and where the
+  // tile kernel's down items (token tiles x row blocks) are too few for its
+  // persistent grid: with a few long items per workgroup, the last round
+  // of items leaves most workgroups idle
+  p.n_split = std::max(ns, 1);
+  if (p.nt_routed == 0) {
+    const int64_t rb = cdiv(L->d_model, kTileWaves * kTileWaveRows<1>);
+    int64_t items = (cdiv(Tk, kTileTok) + E / 2) * rb;   // Zipf-skewed segments: about E/2 extra partial tiles
+    if (S > 0 && p.nt_shared == 0) items += S * cdiv(T, kTileTok) * rb;
+    const int gdown = fmin / g;
+    int nsd = 1;
+    while (nsd < kTileSplitMax && items * nsd < static_cast<int64_t>(kTileItemsPerWg) * tile_grid() &&
+           gdown / (nsd + 1) >= kTileSplitMinGroups)
+      nsd++;
+    p.n_split = nsd;
+  }
   const int64_t hcols = Tk * L->d_ff + static_cast<int64_t>(S) * T * L->d_ff_shared;
   p.xsum_bytes = align256(sizeof(float) * static_cast<size_t>(rows) * (L->d_model / g));
   p.h_bytes = align256(sizeof(uint16_t) * static_cast<size_t>(hcols));
@@ -186,26 +221,13 @@ int64_t stream_grid(const WgMap& m) {
   return static_cast<int64_t>(m.n_r) * m.n_sw * m.m_r + (m.n_ent > 0 ? m.ent_start[m.n_ent] : 0);
 }
 
-TileMap tile_map(const moe_layer_t* L, bool shared) {
+TileMap tile_map(const moe_layer_t* L, bool shared, int n_split) {
   TileMap m{};
   m.e0 = shared ? L->n_experts : 0;
   m.n_e = shared ? L->n_shared : L->n_experts;
+  m.n_split = n_split;
   for (int i = 0; i < m.n_e; i++) m.bits[i] = static_cast<int8_t>(L->bits_host[m.e0 + i]);
   return m;
-}
-
-// Persistent tile grid: one workgroup per compute unit (the tile kernel runs
-// one wave per SIMD), a multiple of the XCD count.
-int tile_grid() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cached[dev] == 0) {
-    int cu = 0;
-    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
-    cached[dev] = std::max(kXcds, cu / kXcds * kXcds);
-  }
-  return cached[dev];
 }
 
 // One kernel launch of a stage; `start` / `stop` (may be null) are HIP events
@@ -268,7 +290,7 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   // tile path: plan kernel, then the persistent tile kernel, for one expert set
   auto add_tile = [&](std::vector<Launch>& v, auto nk, bool shared) {
     constexpr int NK = decltype(nk)::value;
-    const TileMap m = tile_map(L, shared);
+    const TileMap m = tile_map(L, shared, NK == 1 ? p.n_split : 1);
     const int32_t* pf = prefix;
     prefix += MOE_MAX_EXPERTS + 1;
     if (m.n_e == 0) return;
@@ -317,16 +339,7 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     else if (ss) hs(a.Tk, a.rows);
   }
   if (p.nt_routed == 0) add_tile(down, one{}, false);
-  if (S > 0 && p.nt_shared == 0) {
-    if (p.n_split > 1) {   // K splits exist only where routed rows stream: tiled shared rows need cleared slices
-      const int64_t off0 = static_cast<int64_t>(a.Tk) * a.d, n = static_cast<int64_t>(a.rows - a.Tk) * a.d;
-      const int64_t total = n * (p.n_split - 1);
-      down.push_back([=, &a](hipEvent_t e0, hipEvent_t e1) {
-        klaunch(zero_slices_kernel, dim3(static_cast<unsigned>(cdiv(total, 256))), dim3(256), s, e0, e1, a, off0, n);
-      });
-    }
-    add_tile(down, one{}, true);
-  }
+  if (S > 0 && p.nt_shared == 0) add_tile(down, one{}, true);
   add_stream(down, one{}, p.n_split);
   issue(xsum, event(0), nullptr, s);
   issue(gate_up, event(1), event(2), s);

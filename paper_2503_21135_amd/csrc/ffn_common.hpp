@@ -37,7 +37,7 @@ struct FfnArgs {
   float* hsum;         // [max(f,fs)/g][rows] group sums of h rows
   float* o;
   int64_t split_stride;
-  int n_split_out;     // slices of o the combine adds (zero_slices_kernel clears tiled rows)
+  int n_split_out;     // K slices of the down projection: slices of o the combine adds
   int32_t* tile_prefix;   // workspace: 4 x (MOE_MAX_EXPERTS + 1) item prefixes
   const uint16_t* x16;  // [T][d] fp16 copy of x (tile kernel; row of permuted row p: perm[p])
   int32_t* status;      // device status word or null: MOE_ERR_RANGE when an fp16 operand overflows
@@ -300,6 +300,7 @@ constexpr int kSuper = 8;
 // Experts e0 .. e0+n_e-1 of one tile launch; bits[e - e0].
 struct TileMap {
   int e0, n_e;
+  int n_split;   // K slices per item (down projection; 1 for gate/up)
   int8_t bits[MOE_MAX_EXPERTS];
 };
 
@@ -316,8 +317,6 @@ group_sum_kernel(FfnArgs a, const uint16_t* __restrict__ in, const int32_t* __re
                  int64_t ld, int p0, int p1, int K, int p_split, int K2, float* __restrict__ out);
 
 __global__ void __launch_bounds__(256) gather_f16_kernel(FfnArgs a, int T);
-
-__global__ void __launch_bounds__(256) zero_slices_kernel(FfnArgs a, int64_t off0, int64_t n);
 
 template <int NK>
 __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, int32_t* __restrict__ prefix);

@@ -79,17 +79,5 @@ template __global__ void group_sum_kernel<2>(FfnArgs, const uint16_t*, const int
 template __global__ void group_sum_kernel<4>(FfnArgs, const uint16_t*, const int32_t*, int64_t, int, int, int,
                                              int, int, float*);
 
-// ------------------------------------------------------------------ split slices
-// Zeros slices 1 .. n_split_out-1 of o over the floats [off0, off0 + n) of a
-// slice: the rows the tile kernel writes into slice 0 only, where the
-// streaming kernel's K splits make the combine add several slices.
-__global__ void __launch_bounds__(256) zero_slices_kernel(FfnArgs a, int64_t off0, int64_t n) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t total = n * (a.n_split_out - 1);
-  if (i >= total) return;
-  const int64_t sp = 1 + i / n;
-  a.o[sp * a.split_stride + off0 + i % n] = 0.f;
-}
-
 }  // namespace ffn
 }  // namespace moe

@@ -109,8 +109,9 @@ __device__ __forceinline__ TileWaves<NK> tile_waves(const FfnArgs& a, int e, int
   return w;
 }
 
-// Items of expert e: (row blocks of eight waves) x (token tiles); the
-// exclusive prefix over the launch's experts goes to prefix[0 .. n_e].
+// Items of expert e: (row blocks of eight waves) x (token tiles) x (K
+// slices); the exclusive prefix over the launch's experts goes to
+// prefix[0 .. n_e].
 template <int NK>
 __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, int32_t* __restrict__ prefix) {
   __shared__ int cnt[MOE_MAX_EXPERTS];
@@ -122,7 +123,7 @@ __global__ void __launch_bounds__(256) tile_plan_kernel(FfnArgs a, TileMap map, 
     const int tiles = (n_tok + kTileTok - 1) / kTileTok;
     const int R = NK == 1 ? a.d : (e < a.E ? a.f : a.fs);
     const TileWaves<NK> w = tile_waves<NK, false>(a, e, R);
-    items = tiles * ((w.pre[TileWaves<NK>::NC] + kTileWaves - 1) / kTileWaves);
+    items = tiles * ((w.pre[TileWaves<NK>::NC] + kTileWaves - 1) / kTileWaves) * map.n_split;
   }
   if (i < MOE_MAX_EXPERTS) cnt[i] = items;
   __syncthreads();
@@ -288,7 +289,7 @@ __device__ __forceinline__ TSrc tile_src(const FfnArgs& a, int kind, bool copy, 
 // the same in every wave of the workgroup.
 template <int NM2, int NK, int NS, int BW0, int BW1, int TB>
 __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, int e, bool copy0, bool copy1, int be,
-                                          int wpos, int wend, int R, int t0, int t1) {
+                                          int wpos, int wend, int R, int t0, int t1, int sp, int n_split) {
   constexpr int g = NM2 * 16;
   constexpr int SPT = TileStage<NM2>::SPT;
   // activation slots of the tile's TB token blocks, and loads per thread and
@@ -308,7 +309,8 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
   const int n = lane & 31, kh = lane >> 5;
   const bool routed = e < a.E;
   const int K = down ? (routed ? a.f : a.fs) : a.d;
-  const int G = K / g;
+  // the item's groups of K: [g0, g1), slice sp of n_split
+  const int g0 = sp * (K / g) / n_split, g1 = (sp + 1) * (K / g) / n_split;
   const int32_t* order = down ? a.order_dn : a.order_gu;
   const bool wlive = wpos < wend;   // wave-uniform: a wave without positions only stages and waits
   const int q0 = wpos + n, q1 = down ? q0 + 32 : q0;
@@ -334,7 +336,7 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
                   : kOOB;
   }
   auto stage_a = [&](int buf, int gi) {
-    const bool gv = gi < G;
+    const bool gv = gi < g1;
     const uint32_t adv = gv ? 2u * static_cast<uint32_t>(gi * g) : 0u;
     u32x4* st = stage_of(lds, buf);
 #pragma unroll
@@ -354,21 +356,21 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
   HCodes<NM2, BW0> c0[NS];
   HCodes<NM2, BW1> c1[NS];
   auto load = [&](HCodes<NM2, BW0>& x0, HCodes<NM2, BW1>& x1, int gi) {
-    hload<NM2, BW0>(x0, src0, gi, gi < G);
-    hload<NM2, BW1>(x1, src1, gi, gi < G);
+    hload<NM2, BW0>(x0, src0, gi, gi < g1);
+    hload<NM2, BW1>(x1, src1, gi, gi < g1);
   };
-  stage_a(0, 0);
-  load(c0[0], c1[0], 0);
-  if constexpr (NS == 3) stage_a(1, 1);
-  load(c0[1], c1[1], 1);
-  if constexpr (NS == 3) load(c0[2], c1[2], 2);
+  stage_a(0, g0);
+  load(c0[0], c1[0], g0);
+  if constexpr (NS == 3) stage_a(1, g0 + 1);
+  load(c0[1], c1[1], g0 + 1);
+  if constexpr (NS == 3) load(c0[2], c1[2], g0 + 2);
   hwait_vm<WAITN, NS, 1>();   // codes and activations of group 0 have landed (this wave's share)
   tile_barrier();      // ... every wave's share
 
   auto group = [&](HCodes<NM2, BW0>& x0, HCodes<NM2, BW1>& x1, int buf, int gi) {
     // that stage was last read for group gi-1 (barrier since)
     stage_a((buf + NS - 1) % NS, gi + NS - 1);
-    if (gi < G && wlive) {   // workgroup-uniform G (odd for some shapes), wave-uniform wlive
+    if (gi < g1 && wlive) {   // workgroup-uniform g1 (odd group counts), wave-uniform wlive
       const u32x4* st = stage_of(lds, buf);
       // the slot of K-step s and token block tb is a0 ^ s plus 32*SPT*tb
       // (n % SPT is the swizzle of every token block, and s < NM2 touches
@@ -416,7 +418,7 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
     hwait_vm<WAITN, NS, 0>();   // everything but the newer loads: group gi+1's codes and activations
     tile_barrier();
   };
-  for (int gi = 0; gi < G; gi += NS) {
+  for (int gi = g0; gi < g1; gi += NS) {
     group(c0[0], c1[0], 0, gi);
     group(c0[1], c1[1], 1, gi + 1);
     if constexpr (NS == 3) group(c0[2], c1[2], 2, gi + 2);
@@ -445,9 +447,9 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
       }
     if (bad && a.status) *a.status = MOE_ERR_RANGE;
   } else {
-    // slice 0 of o; the host clears the other split slices of tiled rows
-    float* ob0 = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row0;
-    float* ob1 = a.o + static_cast<int64_t>(t0 + 4 * kh) * R + row1;
+    // slice sp of o (the combine adds the slices)
+    float* ob0 = a.o + sp * a.split_stride + static_cast<int64_t>(t0 + 4 * kh) * R + row0;
+    float* ob1 = a.o + sp * a.split_stride + static_cast<int64_t>(t0 + 4 * kh) * R + row1;
 #pragma unroll
     for (int tb = 0; tb < TB; tb++)
 #pragma unroll
@@ -468,13 +470,13 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
 // partial) picks one, two or four 32-token blocks.
 template <int NM2, int NK, int B>
 __device__ __forceinline__ void tile_dispatch(const FfnArgs& a, const TileLds& lds, int e, int cls, bool base_item,
-                                              int wpos, int wend, int R, int t0, int t1) {
+                                              int wpos, int wend, int R, int t0, int t1, int sp, int n_split) {
   const int nt = t1 - t0;
   auto by_tb = [&](auto ns, auto w0, auto w1, bool c0, bool c1) {
     constexpr int NS = decltype(ns)::value, W0 = decltype(w0)::value, W1 = decltype(w1)::value;
-    if (nt <= 32) tile_item<NM2, NK, NS, W0, W1, 1>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1);
-    else if (nt <= 64) tile_item<NM2, NK, NS, W0, W1, 2>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1);
-    else tile_item<NM2, NK, NS, W0, W1, 4>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1);
+    if (nt <= 32) tile_item<NM2, NK, NS, W0, W1, 1>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1, sp, n_split);
+    else if (nt <= 64) tile_item<NM2, NK, NS, W0, W1, 2>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1, sp, n_split);
+    else tile_item<NM2, NK, NS, W0, W1, 4>(a, lds, e, c0, c1, B, wpos, wend, R, t0, t1, sp, n_split);
   };
   using WB = std::integral_constant<int, B>;
   using W8 = std::integral_constant<int, 8>;
@@ -518,7 +520,7 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
       if (pre[mid] <= item) lo = mid; else hi = mid - 1;
     }
     const int e = map.e0 + lo;
-    const int local = item - pre[lo];
+    int local = item - pre[lo];
     const int seg0 = uni(a.offsets[e]), seg1 = uni(a.offsets[e + 1]);
     const int tiles = (seg1 - seg0 + kTileTok - 1) / kTileTok;
     const bool routed = e < a.E;
@@ -528,8 +530,11 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     constexpr int NC = TileWaves<NK>::NC;
     const int n_w = w.pre[NC];
     const int n_rb = (n_w + kTileWaves - 1) / kTileWaves;
-    // (row block, token tile) of the local index: super-rows of kSuper row
-    // blocks, token tiles outer and row blocks inner within a super-row
+    // (K slice, row block, token tile) of the local index: slices outermost;
+    // within a slice super-rows of kSuper row blocks, token tiles outer and
+    // row blocks inner within a super-row
+    const int sp = local / (n_rb * tiles);
+    local -= sp * n_rb * tiles;
     const int full = (n_rb / kSuper) * kSuper * tiles;
     int rb, tt;
     if (local < full) {
@@ -554,14 +559,15 @@ ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
     const bool base_item = min((rb + 1) * kTileWaves, n_w) <= w.pre[1];
     const int t0 = seg0 + tt * kTileTok, t1 = min(t0 + kTileTok, seg1);
     const int B = map.bits[e - map.e0];
-    if (B == 8) tile_dispatch<NM2, NK, 8>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
+    if (B == 8) tile_dispatch<NM2, NK, 8>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1, sp, map.n_split);
     else if (NM2 == 4 && B == 16) {   // unquantized experts need group 64
-      if constexpr (NM2 == 4) tile_dispatch<NM2, NK, 16>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
-    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
-    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
+      if constexpr (NM2 == 4)
+        tile_dispatch<NM2, NK, 16>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1, sp, map.n_split);
+    } else if (B == 4) tile_dispatch<NM2, NK, 4>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1, sp, map.n_split);
+    else if (B == 2) tile_dispatch<NM2, NK, 2>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1, sp, map.n_split);
     else if constexpr (NM2 % 4 == 0) {
-      if (B == 6) tile_dispatch<NM2, NK, 6>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
-      else tile_dispatch<NM2, NK, 3>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1);
+      if (B == 6) tile_dispatch<NM2, NK, 6>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1, sp, map.n_split);
+      else tile_dispatch<NM2, NK, 3>(a, lds, e, cls, base_item, wpos, wend, R, t0, t1, sp, map.n_split);
     }
     tile_barrier();   // the LDS stages are reused by the next item
   }

@@ -293,8 +293,8 @@ def test_tile_sets_with_split_k(orc):
 def test_shared_tile_beside_split_k(orc):
     # 16 routed experts at ~75 tokens stream over 32-token tile sets with the
     # down projection split over K, while the shared expert sees all 600
-    # tokens and goes to the tile kernel: the tile kernel writes slice 0 of
-    # its rows and the other slice of those rows must be zero for the
+    # tokens and goes to the tile kernel, whose down items take the same K
+    # slices: every slice of every row must be written by this call for the
     # combine's sum
     import dataclasses
     import paper_2503_21135_amd as P
@@ -315,7 +315,9 @@ def test_shared_tile_beside_split_k(orc):
     b.o.fill_(123.0)
     y, b = _run(layer, x)
     Tk = T * cfg.top_k
-    assert torch.count_nonzero(b.o[1, Tk:]).item() == 0
+    rows = T * (cfg.top_k + cfg.n_shared)
+    assert torch.count_nonzero(b.o[:, :rows] == 123.0).item() == 0
+    assert torch.count_nonzero(b.o[1, Tk:rows]).item() > 0   # the shared rows' second K slice
     res = orc.layer_forward(inp, x, row_slot=rs)
     routing_matches(layer, res, b)
     err = rel_l2(y, res["y"])
