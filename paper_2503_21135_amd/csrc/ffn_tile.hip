@@ -50,6 +50,9 @@ namespace ffn {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
@@ -426,39 +429,58 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
   hwait_vm<0, 0, 0>();
   if (!wlive) return;
 
-  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4
+  // outputs: tokens t0 + 32*tb + 8*(r/4) + 4*kh + r%4, stored through a
+  // buffer resource over the tile's rows (the token's part of the offset is
+  // the scalar offset; a lane's offset is kOOB past its class or, in a
+  // partial tile, past the segment, which drops the store)
+  const int lim = t1 - t0 - 4 * kh;   // the lane's tokens t0 + 4*kh + dt exist for dt < lim
+  const bool full = t1 - t0 == 32 * TB;   // workgroup-uniform
   if constexpr (!down) {
     // rows of one item are all routed or all shared: one h row width
     const int hw = t0 < a.Tk ? a.f : a.fs;
-    uint16_t* hbase = a.h + h_row(a, t0 + 4 * kh) + row0;
-    bool bad = false;
+    const Rsrc hr = make_rsrc(a.h + h_row(a, t0), static_cast<uint32_t>(kTileTok * hw * 2));
+    const uint32_t off = live0 ? 2u * static_cast<uint32_t>(4 * kh * hw + row0) : kOOB;
+    uint32_t hmax = 0u;   // running maximum of the fp16 magnitudes (bit patterns), per half
 #pragma unroll
     for (int tb = 0; tb < TB; tb++)
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
-        if (live0 && t0 + 4 * kh + dt < t1) {
-          // h = bf16(silu(g) * u), stored as its fp16 value (exact unless
-          // it is below 2^-17 in magnitude or beyond fp16's range)
-          const float hb = __uint_as_float(bf16_rne(silu_mul_fast(acc0[tb][r], acc1[tb][r])) << 16);
-          hbase[dt * hw] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hb));
-          bad = bad || !fp16_finite(hb);
-        }
+      for (int r = 0; r < 16; r += 2) {
+        const int dt = tb * 32 + 8 * (r / 4) + (r % 4);   // element r + 1 is token dt + 1
+        // h = bf16(silu(g) * u) (round to nearest even), stored as its fp16
+        // value: exact unless below 2^-17 in magnitude or beyond fp16's range
+        const f32x2 v = {silu_mul_fast(acc0[tb][r], acc1[tb][r]), silu_mul_fast(acc0[tb][r + 1], acc1[tb][r + 1])};
+        const uint32_t hb = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+        const f32x2 hv = {bf16_lo(hb), bf16_hi(hb)};
+        const uint32_t h16 = __builtin_bit_cast(uint32_t, __builtin_convertvector(hv, f16x2));
+        hmax = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, hmax),
+                                                                      __builtin_bit_cast(u16x2, h16 & 0x7FFF7FFFu)));
+        const uint32_t o0 = (full || dt < lim) ? off : kOOB, o1 = (full || dt + 1 < lim) ? off : kOOB;
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h16), hr, o0, static_cast<uint32_t>(dt * hw * 2), 0);
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h16 >> 16), hr, o1,
+                                              static_cast<uint32_t>((dt + 1) * hw * 2), 0);
       }
-    if (bad && a.status) *a.status = MOE_ERR_RANGE;
+    // fp16 infinity or NaN (0x7C00 and above) where a stored value did not fit;
+    // values a lane does not store come from zero accumulators or rows past
+    // the segment, whose h is never read, so they take part in the check too
+    if (live0 && ((hmax & 0xFFFFu) >= 0x7C00u || (hmax >> 16) >= 0x7C00u) && a.status) *a.status = MOE_ERR_RANGE;
   } else {
     // slice sp of o (the combine adds the slices)
-    float* ob0 = a.o + sp * a.split_stride + static_cast<int64_t>(t0 + 4 * kh) * R + row0;
-    float* ob1 = a.o + sp * a.split_stride + static_cast<int64_t>(t0 + 4 * kh) * R + row1;
+    const Rsrc orc = make_rsrc(a.o + sp * a.split_stride + static_cast<int64_t>(t0) * R,
+                               static_cast<uint32_t>(kTileTok * R * 4));
+    const uint32_t off0 = live0 ? 4u * static_cast<uint32_t>(4 * kh * R + row0) : kOOB;
+    const uint32_t off1 = live1 ? 4u * static_cast<uint32_t>(4 * kh * R + row1) : kOOB;
 #pragma unroll
     for (int tb = 0; tb < TB; tb++)
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const int dt = tb * 32 + 8 * (r / 4) + (r % 4);
-        if (t0 + 4 * kh + dt < t1) {
-          if (live0) ob0[dt * R] = acc0[tb][r];
-          if (live1) ob1[dt * R] = acc1[tb][r];
-        }
+        const bool ok = full || dt < lim;
+        const uint32_t so = static_cast<uint32_t>(dt * R * 4);
+        // through float temporaries: a bit cast of a vector element itself
+        // takes element 0 in this compiler
+        const float v0 = acc0[tb][r], v1 = acc1[tb][r];
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), orc, ok ? off0 : kOOB, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), orc, ok ? off1 : kOOB, so, 0);
       }
   }
 }
