@@ -310,7 +310,7 @@ def test_shared_tile_beside_split_k(orc):
     layer.set_epoch(0)
     rs = oracle_row_slots(orc, inp)
     x = mi.make_x(cfg, T, stream=970)
-    # garbage in every slice first: the zeros must come from this call
+    # garbage in every slice first: every value must come from this call
     b = layer.buffers(T)
     b.o.fill_(123.0)
     y, b = _run(layer, x)
@@ -322,6 +322,39 @@ def test_shared_tile_beside_split_k(orc):
     routing_matches(layer, res, b)
     err = rel_l2(y, res["y"])
     print("shared tile + split-K", "rel_l2", err, flush=True)
+    assert err <= TOL and err <= DIAG_TILE
+
+
+def test_tile_down_split_k(orc):
+    # 4 routed experts at ~300 tokens each go to the tile kernel, whose down
+    # items (a few token tiles x one 512-row block) are too few for its
+    # persistent grid, so the plan splits the down projection over K: d_ff
+    # 2048 at group 128, two slices of 8 groups, each writing its own slice
+    # of o.  The slices must add up to the oracle's rows segment by segment.
+    import dataclasses
+    import paper_2503_21135_amd as P
+    from paper_2503_21135_amd import api
+    cfg = dataclasses.replace(mi.TINY6, name="tile-down-splitk", cfg_id=9, n_experts=4, n_shared=0,
+                              d_model=512, d_ff=2048, bits_literal=(8, 4, 6, 2))
+    inp = mi.LayerInputs(cfg)
+    layer = P.MoELayer(inp)
+    T = 600
+    n_split, _ = api.moe_ffn_plan(layer.desc, T, cfg.top_k)
+    assert n_split == 2
+    layer.set_epoch(0)
+    rs = oracle_row_slots(orc, inp)
+    x = mi.make_x(cfg, T, stream=980)
+    b = layer.buffers(T)
+    b.o.fill_(123.0)
+    y, b = _run(layer, x)
+    rows = T * cfg.top_k
+    assert torch.count_nonzero(b.o[:, :rows] == 123.0).item() == 0
+    assert torch.count_nonzero(b.o[1, :rows]).item() > 0   # the second K slice holds partial sums
+    res = orc.layer_forward(inp, x, row_slot=rs)
+    routing_matches(layer, res, b)
+    worst = check_segments(res, gpu_o_rows(b, res["o_rows"]), bound=DIAG_TILE)
+    err = rel_l2(y, res["y"])
+    print("tile down split-K", np.diff(res["offsets"]).tolist(), "worst segment", worst, "rel_l2", err, flush=True)
     assert err <= TOL and err <= DIAG_TILE
 
 
