@@ -39,9 +39,10 @@ namespace ffn {
 // class of the row order -- base codes, or copies for the gate, the up or both
 // rows -- starts a new wave), and eight consecutive waves form a row block;
 // a wave's class picks its sources, so a small class costs one wave, not a
-// workgroup.  Work items (expert, row block, token tile) come from a prefix
-// table a small plan kernel builds from the routing offsets and class
-// counts, and are spread over a persistent grid so that the workgroups of one
+// workgroup.  Work items (expert, row block, token tile; a down item also
+// takes a K slice and writes its own slice of o, which the combine adds) come
+// from a prefix table a small plan kernel builds from the routing offsets and
+// class counts, and are spread over a persistent grid so that the workgroups of one
 // XCD (hardware places workgroup b on XCD b % 8) take consecutive items.  Within an expert
 // the items run in super-tiles of kSuper row blocks x kSuper token tiles, so
 // that the workgroups one XCD runs together share both their code rows and
