@@ -18,8 +18,9 @@ namespace ffn {
 // and the accumulation runs over the whole K with no per-group epilogue.
 //
 // Dequantization: a code q OR-ed into the mantissa of fp16 1024.0 gives
-// exactly 1024 + q (q < 1024); one packed fp16 subtraction of 1024 + z makes
-// q - z exactly, one packed fp16 multiplication by s rounds the product.
+// exactly 1024 + q (q < 1024; 8-bit codes: one byte permute against bytes of
+// 0x64 per pair); one packed fp16 subtraction of 1024 + z makes q - z
+// exactly, one packed fp16 multiplication by s rounds the product.
 //
 // Eight waves per workgroup, two per SIMD.  Each wave owns two weight rows
 // per lane column -- the gate and the up row of 32 positions (gate/up), or
@@ -42,11 +43,11 @@ namespace ffn {
 // workgroup.  Work items (expert, row block, token tile; a down item also
 // takes a K slice and writes its own slice of o, which the combine adds) come
 // from a prefix table a small plan kernel builds from the routing offsets and
-// class counts, and are spread over a persistent grid so that the workgroups of one
-// XCD (hardware places workgroup b on XCD b % 8) take consecutive items.  Within an expert
-// the items run in super-tiles of kSuper row blocks x kSuper token tiles, so
-// that the workgroups one XCD runs together share both their code rows and
-// their activation rows through that XCD's L2.
+// class counts, and are spread over a persistent grid so that the workgroups
+// of one XCD (hardware places workgroup b on XCD b % 8) take consecutive
+// items.  Within an expert the items run in super-tiles of kSuper row blocks
+// x kSuper token tiles, so that the workgroups one XCD runs together share
+// both their code rows and their activation rows through that XCD's L2.
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
