@@ -30,8 +30,14 @@ struct Plan {
 // 389 us against the tile kernel's few items).
 constexpr int kSharedSplitMax = 512;
 // Routed experts expecting up to this many tokens stream too, with
-// workgroup sets taking every n_tt-th 32-token tile of the expert.
+// workgroup sets taking every n_tt-th 32-token tile of the expert -- where the
+// experts are narrow (d_ff below kTileWideFf).  Wide experts give the tile
+// kernel enough row blocks to fill its grid at any token count, and there it
+// is faster from 29 tokens per expert (Mixtral-shaped layer, 32 to 96 tokens
+// per expert: FFN 4-30 % faster; the Qwen-shaped layer, d_ff 1408, at 34
+// tokens per expert: 13 % slower).
 constexpr int kRoutedSplitMax = 96;
+constexpr int kTileWideFf = 4096;
 
 // Persistent tile grid: one workgroup of eight waves per compute unit (two
 // waves per SIMD), a multiple of the XCD count.
@@ -50,7 +56,7 @@ int tile_grid() {
 // Split-K of the tile kernel's down projection: slices (at most
 // kTileSplitMax, each at least kTileSplitMinGroups groups of K) until the
 // estimated items reach kTileItemsPerWg per workgroup of the grid.
-constexpr int kTileSplitMax = 4;
+constexpr int kTileSplitMax = 8;
 constexpr int kTileItemsPerWg = 4;
 constexpr int kTileSplitMinGroups = 8;
 
@@ -78,7 +84,7 @@ Plan make_plan(const moe_layer_t* L, int T, int k) {
   ns = std::min(ns, std::max(1, gmin / 8));
   p.nt_routed = pick_nt(static_cast<double>(Tk) / E);
   p.tt_routed = 1;
-  if (p.nt_routed == 0 && Tk <= static_cast<int64_t>(kRoutedSplitMax) * E) {
+  if (p.nt_routed == 0 && Tk <= static_cast<int64_t>(kRoutedSplitMax) * E && L->d_ff < kTileWideFf) {
     // a few dozen tokens per expert: 32-token tiles over several workgroup
     // sets (one more than the mean needs, for skewed loads)
     p.nt_routed = 2;

@@ -31,7 +31,7 @@ DIAG_TILE = 1.5e-3   # rows through the fp16 tile kernel
 
 def _layer(name):
     import paper_2503_21135_amd as P
-    wk = mi.WORKLOADS[name]
+    wk = mi.WORKLOADS[name] if isinstance(name, str) else name
     inp = mi.LayerInputs(wk.layer)
     return wk, inp, P.MoELayer(inp)
 
@@ -138,8 +138,11 @@ def check_segments(res, o_gpu, bound=TOL):
     return worst
 
 
-def _sampled_parity(orc, name, n_extra, seed=0):
+def _sampled_parity(orc, name, n_extra, seed=0, n_split=None):
     wk, inp, layer = _layer(name)
+    if n_split is not None:
+        from paper_2503_21135_amd import api
+        assert api.moe_ffn_plan(layer.desc, wk.tokens, wk.layer.top_k)[0] == n_split
     layer.set_epoch(0)
     rs = oracle_row_slots(orc, inp)
     batch = mi.make_batch(wk, inp)
@@ -147,6 +150,7 @@ def _sampled_parity(orc, name, n_extra, seed=0):
     _, ids, _ = orc.route(batch.x, inp.router, wk.layer.top_k, batch.bias)
     off, perm, _ = orc.permute(ids, wk.layer.n_experts, wk.layer.n_shared)
     toks = segment_sample(off, perm, wk.tokens, n_extra, seed)
+    name = wk.name
     print(name, "oracle on", len(toks), "tokens covering every expert segment", flush=True)
     res = orc.layer_forward(inp, batch.x, bias=batch.bias, row_slot=rs, tokens=toks)
     routing_matches(layer, res, b)
@@ -189,6 +193,15 @@ def test_mixtral_prefill_parity(orc):
     # 4096 tokens, Zipf-skewed loads: experts with up to ~3300 rows, many
     # 128-token tiles per expert; every expert's first and last rows checked
     assert _sampled_parity(orc, "mixtral-prefill", 16) <= DIAG_TILE
+
+
+def test_mixtral_mid_batch_parity(orc):
+    # 192 tokens on the Mixtral-shaped layer: 48 routed tokens per expert, which
+    # the plan sends to the tile kernel (wide experts fill its grid) in 64-token
+    # blocks of partial 128-token tiles, with the down projection split into
+    # eight K slices because its items are few
+    wk = mi.Workload("mixtral-mid", mi.MIXTRAL, 192)
+    assert _sampled_parity(orc, wk, 16, n_split=8) <= DIAG_TILE
 
 
 def test_deepseek_prefill_parity(orc):
