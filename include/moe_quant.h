@@ -79,8 +79,9 @@
  * even) before the down projection, as the paper feeds 16-bit activations to
  * the matrix cores (Sec. V-B); accumulation is fp32.  The weights enter in
  * one of two ways, chosen per launch from the expected tokens per expert:
- *   - up to 96 expected tokens per routed expert, and shared experts over up
- *     to 512 tokens (decode): exactly -- the matrix cores multiply the integer
+ *   - up to 28 expected tokens per routed expert (48 for experts narrower
+ *     than d_ff 4096), and shared experts over up to 512 tokens (decode):
+ *     exactly -- the matrix cores multiply the integer
  *     codes (exact in bf16) by the bf16 activations, and each group's scale
  *     and zero point are applied to the fp32 partial sum;
  *   - more tokens (prefill): as the 16-bit dequantized

@@ -31,12 +31,13 @@ struct Plan {
 constexpr int kSharedSplitMax = 512;
 // Routed experts expecting up to this many tokens stream too, with
 // workgroup sets taking every n_tt-th 32-token tile of the expert -- where the
-// experts are narrow (d_ff below kTileWideFf).  Wide experts give the tile
-// kernel enough row blocks to fill its grid at any token count, and there it
-// is faster from 29 tokens per expert (Mixtral-shaped layer, 32 to 96 tokens
-// per expert: FFN 4-30 % faster; the Qwen-shaped layer, d_ff 1408, at 34
-// tokens per expert: 13 % slower).
-constexpr int kRoutedSplitMax = 96;
+// experts are narrow (d_ff below kTileWideFf; DeepSeek-shaped layer, d_ff
+// 1408: the tile kernel is 13 % slower at 36 tokens per expert, even at 48,
+// 10-25 % faster from 56).  Wide experts give the tile kernel enough row
+// blocks to fill its grid at any token count, and there it is faster from 29
+// tokens per expert (Mixtral-shaped layer, 32 to 96 tokens per expert: FFN
+// 13-32 % faster).
+constexpr int kRoutedSplitMax = 48;
 constexpr int kTileWideFf = 4096;
 
 // Persistent tile grid: one workgroup of eight waves per compute unit (two

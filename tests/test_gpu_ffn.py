@@ -259,14 +259,14 @@ def test_int6_mixtral_shaped_decode_parity(orc):
 
 
 def test_routed_token_tiles_split_skewed(orc):
-    # 200 tokens, top-2 of 8 experts: 50 expected per expert, so the routed
+    # 192 tokens, top-2 of 8 experts: 48 expected per expert, so the routed
     # experts stream with their 32-token tiles spread over three workgroup
-    # sets; the bias piles most tokens on experts 0 and 1 (seven tiles each)
+    # sets; the bias piles most tokens on experts 0 and 1 (six tiles each)
     # and leaves experts 5 and 6 empty
     wk, inp, layer = _layer("tiny")
     layer.set_epoch(0)
     rs = oracle_row_slots(orc, inp)
-    x = mi.make_x(wk.layer, 200, stream=950)
+    x = mi.make_x(wk.layer, 192, stream=950)
     bias = np.array([40, 40, 0, 0, 0, -40, -40, 1], np.float32)
     y, b = _run(layer, x, bias)
     res = orc.layer_forward(inp, x, bias=bias, row_slot=rs)
@@ -304,7 +304,7 @@ def test_tile_sets_with_split_k(orc):
 
 
 def test_shared_tile_beside_split_k(orc):
-    # 16 routed experts at ~75 tokens stream over 32-token tile sets with the
+    # 32 routed experts at ~37 tokens stream over 32-token tile sets with the
     # down projection split over K, while the shared expert sees all 600
     # tokens and goes to the tile kernel, whose down items take the same K
     # slices: every slice of every row must be written by this call for the
@@ -312,8 +312,8 @@ def test_shared_tile_beside_split_k(orc):
     import dataclasses
     import paper_2503_21135_amd as P
     from paper_2503_21135_amd import api
-    bits = (8, 4, 6, 2, 3, 4, 8, 2, 4, 6, 4, 3, 2, 8, 4, 4)
-    cfg = dataclasses.replace(mi.TINY6, name="shared-tile-splitk", cfg_id=8, n_experts=16, n_shared=1,
+    bits = (8, 4, 6, 2, 3, 4, 8, 2, 4, 6, 4, 3, 2, 8, 4, 4) * 2
+    cfg = dataclasses.replace(mi.TINY6, name="shared-tile-splitk", cfg_id=8, n_experts=32, n_shared=1,
                               d_ff=2048, d_ff_shared=2048, bits_literal=bits)
     inp = mi.LayerInputs(cfg)
     layer = P.MoELayer(inp)
