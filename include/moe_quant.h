@@ -282,8 +282,9 @@ int moe_route_permute(const uint16_t* x, int32_t T, int32_t d,
 /*
  * moe_route_workspace_bytes -- bytes of device workspace moe_route_permute
  * needs for this batch: two int32 [ceil(T/64)][E] tables (per-chunk expert
- * counts and bases) and, from 256 tokens on, the fp32 [T][E] logits of the
- * large-batch router, each region 256-byte aligned.  Returns 0 for T < 0 or
+ * counts and bases) and, from 256 tokens or 16 experts on, the fp32 [T][E]
+ * logits that the router writes before its top-k pass, each region 256-byte
+ * aligned.  Returns 0 for T < 0 or
  * E <= 0.  The contents need no initialization and are scratch between calls.
  */
 size_t moe_route_workspace_bytes(int32_t T, int32_t E, int32_t k, int32_t S);

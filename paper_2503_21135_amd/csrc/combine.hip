@@ -7,6 +7,13 @@
 namespace moe {
 namespace {
 
+// One thread per 4 columns of a token.  The token's rows are taken in
+// batches of NB (2, 4 or 8, the smallest that holds the k + S rows, else 8):
+// the row indices, then the rows of the batch are loaded before the first add,
+// so the loads overlap instead of waiting on each other; the adds keep the
+// fixed order (slices ascending per row, then rows ascending into the fused
+// multiply-add chain).
+template <int NB>
 __global__ void __launch_bounds__(256)
 combine_kernel(const float* __restrict__ o, int n_split, int64_t ss, const int32_t* __restrict__ inv,
                const float* __restrict__ w, int T, int k, int S, int d, float* __restrict__ y) {
@@ -15,18 +22,37 @@ combine_kernel(const float* __restrict__ o, int n_split, int64_t ss, const int32
   if (id >= static_cast<int64_t>(T) * per) return;
   const int t = static_cast<int>(id / per);
   const int c4 = static_cast<int>(id % per);
-  const int32_t* iv = inv + static_cast<int64_t>(t) * (k + S);
+  const int n = k + S;
+  const int32_t* iv = inv + static_cast<int64_t>(t) * n;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int j = 0; j < k + S; j++) {
-    const int64_t p = iv[j];
-    f32x4 v = reinterpret_cast<const f32x4*>(o + p * d)[c4];
-    for (int sp = 1; sp < n_split; sp++) {
-      const f32x4 u = reinterpret_cast<const f32x4*>(o + sp * ss + p * d)[c4];
-      v = f32x4{v[0] + u[0], v[1] + u[1], v[2] + u[2], v[3] + u[3]};
-    }
-    const float wj = j < k ? w[static_cast<int64_t>(t) * k + j] : 1.0f;
+  for (int j0 = 0; j0 < n; j0 += NB) {
+    int64_t p[NB];
+    float wj[NB];
+    f32x4 v[NB];
 #pragma unroll
-    for (int c = 0; c < 4; c++) acc[c] = __fmaf_rn(wj, v[c], acc[c]);
+    for (int i = 0; i < NB; i++) {
+      const int j = j0 + i;
+      p[i] = j < n ? static_cast<int64_t>(iv[j]) : 0;
+      wj[i] = j < k ? w[static_cast<int64_t>(t) * k + j] : 1.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < NB; i++)
+      if (j0 + i < n) v[i] = reinterpret_cast<const f32x4*>(o + p[i] * d)[c4];
+    for (int sp = 1; sp < n_split; sp++) {
+      f32x4 u[NB];
+#pragma unroll
+      for (int i = 0; i < NB; i++)
+        if (j0 + i < n) u[i] = reinterpret_cast<const f32x4*>(o + sp * ss + p[i] * d)[c4];
+#pragma unroll
+      for (int i = 0; i < NB; i++)
+        if (j0 + i < n) v[i] = f32x4{v[i][0] + u[i][0], v[i][1] + u[i][1], v[i][2] + u[i][2], v[i][3] + u[i][3]};
+    }
+#pragma unroll
+    for (int i = 0; i < NB; i++)
+      if (j0 + i < n) {
+#pragma unroll
+        for (int c = 0; c < 4; c++) acc[c] = __fmaf_rn(wj[i], v[i][c], acc[c]);
+      }
   }
   reinterpret_cast<f32x4*>(y + static_cast<int64_t>(t) * d)[c4] = acc;
 }
@@ -46,7 +72,15 @@ extern "C" int moe_unpermute_combine(const float* o, int32_t n_split, int64_t sp
   if (!aligned16(o) || !aligned16(y) || (n_split > 1 && split_stride % 4)) return MOE_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t n = static_cast<int64_t>(T) * (d / 4);
-  hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0, s, o,
-                     n_split, split_stride, inv_perm, topk_w, T, k, S, d, y);
+  const dim3 grid(static_cast<unsigned>(cdiv(n, 256)));
+  if (k + S <= 2)
+    hipLaunchKernelGGL(combine_kernel<2>, grid, dim3(256), 0, s, o, n_split, split_stride, inv_perm, topk_w,
+                       T, k, S, d, y);
+  else if (k + S <= 4)
+    hipLaunchKernelGGL(combine_kernel<4>, grid, dim3(256), 0, s, o, n_split, split_stride, inv_perm, topk_w,
+                       T, k, S, d, y);
+  else
+    hipLaunchKernelGGL(combine_kernel<8>, grid, dim3(256), 0, s, o, n_split, split_stride, inv_perm, topk_w,
+                       T, k, S, d, y);
   return launch_status(s);
 }

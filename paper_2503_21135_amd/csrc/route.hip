@@ -197,7 +197,8 @@ route_topk_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __r
 constexpr int kLogitWaves = 4;      // waves of a logits workgroup
 constexpr int kLogitExperts = 8;    // experts of a logits workgroup, two per wave
 constexpr int kLogitTokens = 8;     // tokens of a logits workgroup
-constexpr int kSplitRouterMinT = 256;
+constexpr int kSplitRouterMinT = 256;   // batches from this size: logits, then top k
+constexpr int kSplitRouterMinE = 16;    // smaller batches with this many experts too
 
 // Router logits of large batches with the experts spread over workgroups:
 // workgroup (token block, expert block) computes 8 tokens x 8 experts, wave w
@@ -260,15 +261,183 @@ route_logits_kernel(const uint16_t* __restrict__ x, int T, int d, const float* _
     }
 }
 
-// Top k and weights of the logits rows, one wave per token.
+// Reduce-scatter of the NV per-lane partial logits of a wave (NV a power of
+// two, at most 64): at each offset of the header's halving tree (32, 16, ...,
+// 1) a lane keeps one half of its values, hands the other half to the lane
+// `off` away and adds what it receives, so a pair of lanes adds exactly the
+// tree's operands (partial[l] + partial[l + off]; the two lanes add them in
+// either order, which gives the same bits).  Once a lane holds a single value
+// the remaining offsets are plain butterflies.  Value v ends in the lanes l
+// with l / (64 / NV) == v.
+template <int N, int OFF, int NV>
+__device__ __forceinline__ void tree_scatter(float (&a)[NV], int lane) {
+  if constexpr (OFF >= 1) {
+    if constexpr (N > 1) {
+      constexpr int H = N / 2;
+      const bool hi = (lane & OFF) != 0;
+#pragma unroll
+      for (int i = 0; i < H; i++) {
+        const float send = hi ? a[i] : a[i + H];
+        const float keep = hi ? a[i + H] : a[i];
+        a[i] = keep + __shfl_xor(send, OFF, kWave);
+      }
+      tree_scatter<H, OFF / 2, NV>(a, lane);
+    } else {
+      a[0] = a[0] + __shfl_xor(a[0], OFF, kWave);
+      tree_scatter<1, OFF / 2, NV>(a, lane);
+    }
+  }
+}
+
+// Router logits staged through LDS: workgroup (token block of 4*WT tokens,
+// expert block of WE experts) copies SC-column chunks of its token rows
+// (bf16) and router rows (fp32) into LDS with 16-byte loads,
+// the next chunk's loads in flight while the current one is used; wave w
+// holds the WT x WE logits of tokens 4w.. of the block, lane l adding columns
+// l, l + 64, ... in ascending order with one FMA each (the header's per-lane
+// order), then the halving tree over the lanes (tree_scatter) and the bias.
+// x and wr must be 16-byte aligned; tokens and experts past the ends are
+// clamped (computed, not stored).
+template <int WT, int WE, int SC>
+__global__ void __launch_bounds__(4 * kWave)
+route_logits_lds_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
+                        const float* __restrict__ bias, int E, float* __restrict__ logits) {
+  constexpr int TT = 4 * WT;                       // tokens of the block
+  constexpr int NV = WT * WE;                      // partial logits per lane
+  constexpr int XPT = TT * SC / 8 / 256;   // 16-byte x pieces per thread
+  constexpr int WPT = WE * SC / 4 / 256;   // 16-byte router pieces per thread
+  static_assert(NV <= kWave && (NV & (NV - 1)) == 0 && XPT >= 1 && WPT >= 1, "tile shape");
+  __shared__ __attribute__((aligned(16))) uint16_t xs[TT][SC];
+  __shared__ __attribute__((aligned(16))) float wsh[WE][SC];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int n_eb = (E + WE - 1) / WE;   // expert blocks vary fastest: a token block's
+  const int e0 = static_cast<int>(blockIdx.x % n_eb) * WE;   // workgroups run together
+  const int t0 = static_cast<int>(blockIdx.x / n_eb) * TT;
+  u32x4 xr[XPT] = {}, wrg[WPT] = {};
+  auto load = [&](int c0) {
+#pragma unroll
+    for (int j = 0; j < XPT; j++) {
+      const int i = tid + 256 * j, r = i / (SC / 8), c = c0 + (i % (SC / 8)) * 8;
+      if (c < d)
+        xr[j] = *reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(min(t0 + r, T - 1)) * d + c);
+    }
+#pragma unroll
+    for (int j = 0; j < WPT; j++) {
+      const int i = tid + 256 * j, r = i / (SC / 4), c = c0 + (i % (SC / 4)) * 4;
+      if (c < d)
+        wrg[j] = *reinterpret_cast<const u32x4*>(wr + static_cast<int64_t>(min(e0 + r, E - 1)) * d + c);
+    }
+  };
+  float acc[WT][WE];
+#pragma unroll
+  for (int tb = 0; tb < WT; tb++)
+#pragma unroll
+    for (int e = 0; e < WE; e++) acc[tb][e] = 0.0f;
+  load(0);
+  for (int c0 = 0; c0 < d; c0 += SC) {
+    __syncthreads();   // every wave is done with the previous chunk
+#pragma unroll
+    for (int j = 0; j < XPT; j++) {
+      const int i = tid + 256 * j;
+      *reinterpret_cast<u32x4*>(&xs[i / (SC / 8)][(i % (SC / 8)) * 8]) = xr[j];
+    }
+#pragma unroll
+    for (int j = 0; j < WPT; j++) {
+      const int i = tid + 256 * j;
+      *reinterpret_cast<u32x4*>(&wsh[i / (SC / 4)][(i % (SC / 4)) * 4]) = wrg[j];
+    }
+    __syncthreads();
+    if (c0 + SC < d) load(c0 + SC);
+#pragma unroll
+    for (int i = 0; i < SC / kWave; i++) {
+      if (c0 + kWave * i < d) {   // uniform: d is a multiple of 64
+        const int c = kWave * i + lane;
+        float xv[WT], wv_[WE];
+#pragma unroll
+        for (int tb = 0; tb < WT; tb++) xv[tb] = __uint_as_float(static_cast<uint32_t>(xs[wv * WT + tb][c]) << 16);
+#pragma unroll
+        for (int e = 0; e < WE; e++) wv_[e] = wsh[e][c];
+#pragma unroll
+        for (int tb = 0; tb < WT; tb++)
+#pragma unroll
+          for (int e = 0; e < WE; e++) acc[tb][e] = __fmaf_rn(xv[tb], wv_[e], acc[tb][e]);
+      }
+    }
+  }
+  float a[NV];
+#pragma unroll
+  for (int tb = 0; tb < WT; tb++)
+#pragma unroll
+    for (int e = 0; e < WE; e++) a[tb * WE + e] = acc[tb][e];
+  tree_scatter<NV, kWave / 2, NV>(a, lane);
+  constexpr int per = kWave / NV;   // lanes holding each value
+  const int v = lane / per;
+  const int t = t0 + wv * WT + v / WE, e = e0 + v % WE;
+  if (lane % per == 0 && t < T && e < E) {
+    float r = a[0];
+    if (bias) r = r + bias[e];
+    logits[static_cast<int64_t>(t) * E + e] = r;
+  }
+}
+
+// Top k and weights of the logits rows, one wave per token, by rank: lane l
+// holds logits l, l + 64, ... of the token and counts, for each, the logits
+// that precede it in the order (logit descending, index ascending; a NaN is
+// taken as -inf, so every rank is distinct); a logit of rank j < k is the
+// pick of slot j.  The weights follow select_topk's arithmetic: e_j =
+// cexp(l_j - l_0), S summed over the slots in order, w_j = e_j / S.
 __global__ void __launch_bounds__(4 * kWave)
 route_select_kernel(const float* __restrict__ logits, int T, int E, int k,
                     int32_t* __restrict__ topk_ids, float* __restrict__ topk_w) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  select_topk(logits + static_cast<int64_t>(t) * E, E, k, t, threadIdx.x & 63, topk_ids, topk_w);
+  constexpr int kMaxPer = MOE_MAX_EXPERTS / kWave;
+  __shared__ __attribute__((aligned(16))) float lgs[4][MOE_MAX_EXPERTS];
+  __shared__ float selv[4][MOE_MAX_TOPK], exs[4][MOE_MAX_TOPK];
+  __shared__ int32_t seli[4][MOE_MAX_TOPK];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + wv;
+  const float* src = logits + static_cast<int64_t>(min(t, T - 1)) * E;
+  const int E4 = (E + 3) & ~3;   // padded with -inf, which no logit follows
+  float v[kMaxPer];
+#pragma unroll
+  for (int m = 0; m < kMaxPer; m++) {
+    const int e = m * kWave + lane;
+    float u = e < E ? src[e] : -INFINITY;
+    if (u != u) u = -INFINITY;
+    v[m] = u;
+    if (e < E4) lgs[wv][e] = u;
+  }
+  __syncthreads();
+  int rank[kMaxPer];
+#pragma unroll
+  for (int m = 0; m < kMaxPer; m++) rank[m] = 0;
+  for (int e2 = 0; e2 < E4; e2 += 4) {
+    const f32x4 u = *reinterpret_cast<const f32x4*>(&lgs[wv][e2]);
+#pragma unroll
+    for (int m = 0; m < kMaxPer; m++) {
+      if (m * kWave < E) {   // uniform
+        const int e = m * kWave + lane;
+#pragma unroll
+        for (int q = 0; q < 4; q++) rank[m] += (u[q] > v[m] || (u[q] == v[m] && e2 + q < e)) ? 1 : 0;
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < kMaxPer; m++) {
+    const int e = m * kWave + lane;
+    if (e < E && rank[m] < k) {
+      selv[wv][rank[m]] = v[m];
+      seli[wv][rank[m]] = e;
+    }
+  }
+  __syncthreads();
+  if (lane < k) exs[wv][lane] = lib_exp_nonpos(selv[wv][lane] - selv[wv][0]);
+  __syncthreads();
+  if (t >= T || lane >= k) return;
+  float S = 0.0f;
+  for (int j = 0; j < k; j++) S = S + exs[wv][j];
+  topk_ids[static_cast<int64_t>(t) * k + lane] = seli[wv][lane];
+  topk_w[static_cast<int64_t>(t) * k + lane] = exs[wv][lane] / S;
 }
-
 // One chunk's expert lane masks in LDS: bit l of mask[e] is set when token
 // l of the chunk chose expert e (one LDS atomic OR per choice; OR does not
 // depend on the order of the atomics).  The token's choices stay in
@@ -484,7 +653,8 @@ extern "C" size_t moe_route_workspace_bytes(int32_t T, int32_t E, int32_t k, int
   if (T < 0 || E <= 0) return 0;
   const size_t n_chunks = static_cast<size_t>((T + moe::kChunk - 1) / moe::kChunk);
   // chunk histogram, chunk bases, then the logits [T][E] of large batches
-  const size_t logits = T >= moe::kSplitRouterMinT ? sizeof(float) * static_cast<size_t>(T) * E : 0;
+  const bool split = T >= moe::kSplitRouterMinT || E >= moe::kSplitRouterMinE;
+  const size_t logits = split ? sizeof(float) * static_cast<size_t>(T) * E : 0;
   return 2 * moe::align256(sizeof(int32_t) * (n_chunks > 0 ? n_chunks : 1) * E) + moe::align256(logits);
 }
 
@@ -507,15 +677,31 @@ extern "C" int moe_route_permute(const uint16_t* x, int32_t T, int32_t d, const 
   const size_t half = align256(sizeof(int32_t) * static_cast<size_t>(n_chunks > 0 ? n_chunks : 1) * E);
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + half);
-  if (T >= kSplitRouterMinT) {
-    // large batches: logits over (8-token, 8-expert) workgroups, then the top
-    // k per token (the second launch costs more than it saves on small ones)
-    float* logits = reinterpret_cast<float*>(static_cast<char*>(ws) + 2 * half);
+  const bool staged = aligned16(x) && aligned16(w_router);   // 16-byte row loads
+  float* logits = reinterpret_cast<float*>(static_cast<char*>(ws) + 2 * half);
+  const dim3 blk(4 * kWave);
+  auto n_wg = [&](int tt, int te) { return static_cast<unsigned>(cdiv(T, tt) * cdiv(E, te)); };
+  if (T > 0 && staged && (T >= kSplitRouterMinT || E >= kSplitRouterMinE)) {
+    // logits over (token block, expert block) workgroups staged through LDS,
+    // then the top k per token; on small batches of few experts the second
+    // launch would cost more than it saves (one workgroup per token below)
+    if (E <= 8)                          // 8 tokens x 8 experts
+      hipLaunchKernelGGL((route_logits_lds_kernel<2, 8, 256>), dim3(n_wg(8, 8)), blk, 0, s, x, T, d, w_router,
+                         bias, E, logits);
+    else if (n_wg(16, 16) >= 256)        // 16 tokens x 16 experts
+      hipLaunchKernelGGL((route_logits_lds_kernel<4, 16, 256>), dim3(n_wg(16, 16)), blk, 0, s, x, T, d,
+                         w_router, bias, E, logits);
+    else                                 // small batches: 4 tokens x 8 experts, 1024-column chunks
+      hipLaunchKernelGGL((route_logits_lds_kernel<1, 8, 1024>), dim3(n_wg(4, 8)), blk, 0, s, x, T, d, w_router,
+                         bias, E, logits);
+    hipLaunchKernelGGL(route_select_kernel, dim3(static_cast<unsigned>(cdiv(T, 4))), blk, 0, s, logits, T, E, k,
+                       topk_ids, topk_w);
+  } else if (T >= kSplitRouterMinT) {    // rows off 16-byte alignment: a column per lane
     hipLaunchKernelGGL((route_logits_kernel<kLogitTokens, 16>),
                        dim3(static_cast<unsigned>(cdiv(T, kLogitTokens)), static_cast<unsigned>(cdiv(E, kLogitExperts))),
                        dim3(kLogitWaves * kWave), 0, s, x, T, d, w_router, bias, E, logits);
-    hipLaunchKernelGGL(route_select_kernel, dim3(static_cast<unsigned>(cdiv(T, 4))), dim3(4 * kWave), 0, s,
-                       logits, T, E, k, topk_ids, topk_w);
+    hipLaunchKernelGGL(route_select_kernel, dim3(static_cast<unsigned>(cdiv(T, 4))), blk, 0, s, logits, T, E, k,
+                       topk_ids, topk_w);
   } else if (T > 0) {
     hipLaunchKernelGGL(route_topk_kernel, dim3(static_cast<unsigned>(T)), dim3(kRouteWaves * kWave),
                        0, s, x, T, d, w_router, bias, E, k, topk_ids, topk_w);

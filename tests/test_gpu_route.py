@@ -11,7 +11,7 @@ from gpu_util import dev, to_dev_bf16
 pytestmark = pytest.mark.gpu
 
 
-def gpu_route(x_bits, router, bias, k, S, want_xperm=False):
+def gpu_route(x_bits, router, bias, k, S, want_xperm=False, misalign=False):
     import paper_2503_21135_amd as P
     T, d = x_bits.shape
     E = router.shape[0]
@@ -23,6 +23,10 @@ def gpu_route(x_bits, router, bias, k, S, want_xperm=False):
     inv = torch.full((T, k + S), -7, dtype=torch.int32, device=D)
     ws = torch.empty(max(P.moe_route_workspace_bytes(T, E, k, S), 256), dtype=torch.uint8, device=D)
     x = to_dev_bf16(x_bits)
+    if misalign:   # rows start 2 bytes past a 16-byte boundary
+        buf = torch.empty(T * d + 1, dtype=torch.bfloat16, device=D)
+        buf[1:] = x.reshape(-1)
+        x = buf[1:].view(T, d)
     xp = torch.empty((max(T * (k + S), 1), d), dtype=torch.bfloat16, device=D) if want_xperm else None
     P.moe_route_permute(x, torch.from_numpy(router).to(D),
                         None if bias is None else torch.from_numpy(bias).to(D),
@@ -64,12 +68,28 @@ def test_route_workloads(orc, name):
 
 @pytest.mark.parametrize("T,E,k,S,d", [(1, 8, 2, 0, 256), (65, 8, 8, 0, 256), (130, 64, 6, 2, 128),
                                        (7, 256, 16, 0, 64), (200, 3, 1, 1, 192),
-                                       (1024, 255, 16, 1, 64), (1025, 60, 4, 1, 128)])
+                                       (1024, 255, 16, 1, 64), (1025, 60, 4, 1, 128),
+                                       (300, 20, 3, 1, 320), (257, 5, 2, 0, 192), (520, 9, 2, 0, 576),
+                                       (100, 20, 3, 1, 320), (33, 16, 16, 0, 2112)])
 def test_route_edges(orc, T, E, k, S, d):
     rng = np.random.default_rng(T + E)
     x = mi.bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
     router = (rng.standard_normal((E, d)) * 0.02).astype(np.float32)
     check_route(orc, x, router, None, k, S)
+
+
+@pytest.mark.parametrize("T", [300, 100])
+def test_route_misaligned_rows(orc, T):
+    # token rows off a 16-byte boundary take the routers that read a column
+    # per lane; the results are the same bits
+    E, k, S, d = 20, 3, 1, 320
+    rng = np.random.default_rng(77)
+    x = mi.bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    router = (rng.standard_normal((E, d)) * 0.02).astype(np.float32)
+    g = gpu_route(x, router, None, k, S, misalign=True)
+    lg, ids, w = orc.route(x, router, k, None)
+    assert np.array_equal(g["ids"], ids)
+    assert np.array_equal(g["w"].view(np.uint32), w.view(np.uint32))
 
 
 def test_route_ties_and_empty_experts(orc):
