@@ -19,7 +19,10 @@ namespace ffn {
 //
 // Dequantization: a code q OR-ed into the mantissa of fp16 1024.0 gives
 // exactly 1024 + q (q < 1024; 8-bit codes: one byte permute against bytes of
-// 0x64 per pair); one packed fp16 subtraction of 1024 + z makes q - z
+// 0x64 per pair).  A code sitting higher in the word is OR-ed into a smaller
+// magic M whose mantissa unit falls on its lowest bit (64.0 for a 4-bit code
+// at bit 4; 256.0, 64.0, 16.0 for 2-bit codes at bits 2, 4, 6), which reads
+// M + q with no shift.  One packed fp16 subtraction of M + z makes q - z
 // exactly, one packed fp16 multiplication by s rounds the product.
 //
 // Eight waves per workgroup, two per SIMD.  Each wave owns two weight rows
@@ -61,7 +64,6 @@ __device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const 
                                                  0, 0);
 }
 
-constexpr uint32_t kMagic16 = 0x64006400u;   // two fp16 1024.0
 constexpr uint32_t kHigh64 = 0x64646464u;    // the high byte of fp16 1024.0, in every byte
 
 // One LDS stage of the tile kernel: kTileTok token rows x g columns of fp16
@@ -153,17 +155,26 @@ struct TSrc {
 template <int NM2, int B>
 constexpr int kHalfWords = NM2 * 16 / 2 * B / 32;
 
-// fp16 pair (1024 + q_lo, 1024 + q_hi) from two codes at bit offset sh of
-// each half-word (b <= 8 bits wide, masked by m).
-__device__ __forceinline__ uint32_t unpack16(uint32_t w, int sh, uint32_t m, uint32_t vm) {
-  return ((w >> sh) & m) | vm;
+// Magic fp16 pairs M whose mantissa unit is 1 at the bit offset of a code
+// field: 1024.0 (bits 0..), 256.0 (2..), 64.0 (4..), 16.0 (6..).  A code q
+// OR-ed into the field then reads exactly M + q.
+constexpr uint32_t kMagicAt[4] = {0x64006400u, 0x5C005C00u, 0x54005400u, 0x4C004C00u};
+constexpr float kMagicVal[4] = {1024.0f, 256.0f, 64.0f, 16.0f};
+
+// Magic of component i (weights 2i, 2i+1) of a K-step: 4-bit codes sit at
+// bits 0 and 4 of a byte (1024, 64), 2-bit codes at bits 0, 2, 4, 6 (1024,
+// 256, 64, 16); the other widths use 1024 throughout.
+template <int B>
+constexpr int kMagicOf(int i) {
+  return B == 2 ? i : (B == 4 ? 2 * (i & 1) : 0);
 }
 
 // Component i (weights 2i, 2i+1) of the B fragment of K-step s: two fp16
-// weights s*(q - z) of this lane's row.
+// weights s*(q - z) of this lane's row.  zn[i] = -(M + z) for the magic M of
+// component i, mg the magics in registers.
 template <int NM2, int B>
-__device__ __forceinline__ uint32_t dequant_h1(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, int i, f16x2 zneg,
-                                               f16x2 sc, uint32_t vm) {
+__device__ __forceinline__ uint32_t dequant_h1(const uint32_t (&cw)[(kHalfWords<NM2, B>)], int s, int i,
+                                               const f16x2 (&zn)[4], f16x2 sc, const uint32_t (&mg)[4]) {
   if constexpr (B == 16) {
     // unquantized bf16 weights to fp16, rounding toward zero: exact for every
     // bf16 magnitude in [2^-17, 65504] (its last significand bit is >= 2^-24,
@@ -173,36 +184,47 @@ __device__ __forceinline__ uint32_t dequant_h1(const uint32_t (&cw)[(kHalfWords<
   }
   uint32_t r;
   if constexpr (B == 4) {
-    r = unpack16(cw[s], 4 * i, 0x000F000Fu, vm);
+    // codes at bits 0-3 and 4-7 of each half's low byte (i = 0, 1) and high
+    // byte (i = 2, 3): one shift per K-step word
+    const uint32_t w = i < 2 ? cw[s] : cw[s] >> 8;
+    r = (w & ((i & 1) ? 0x00F000F0u : 0x000F000Fu)) | mg[kMagicOf<4>(i)];
   } else if constexpr (B == 8) {
     // bytes (c0, c2, c1, c3): one byte permute with 0x64 bytes per pair gives
     // (0x64 << 8 | q) = 1024 + q in both halves
     r = __builtin_amdgcn_perm(kHigh64, cw[2 * s + (i >> 1)], (i & 1) ? 0x04030401u : 0x04020400u);
   } else if constexpr (B == 2) {
-    r = unpack16(cw[s >> 1], (s & 1) * 8 + 2 * i, 0x00030003u, vm);
+    // codes at bits 2i, 2i+1 of each half's low byte (even K-steps) or high
+    // byte (odd K-steps)
+    const uint32_t w = (s & 1) ? cw[s >> 1] >> 8 : cw[s >> 1];
+    r = (w & (0x00030003u << (2 * i))) | mg[kMagicOf<2>(i)];
   } else if constexpr (B == 6) {  // per 32-code block: words 0-3 bits 0..3, words 4-5 bits 4..5
     const int blk = 6 * (s >> 2);
     const int q = s & 3;   // octet within the block
     const uint32_t lo = cw[blk + q], hi = cw[blk + 4 + (q >> 1)];
     const int o = (q & 1) * 8;
-    r = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | vm;
+    r = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | mg[0];
   } else {  // 3-bit: per 32-code block words (low plane 0-15, low plane 16-31, high plane)
     const int blk = 3 * (s >> 2);
     const int q = s & 3;   // octet within the block
     const uint32_t lo = cw[blk + (q >> 1)], hi = cw[blk + 2];
     const int pi = 4 * q + i;   // pair index within the block
-    r = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | vm;
+    r = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | mg[0];
   }
-  const f16x2 d = __builtin_bit_cast(f16x2, r) + zneg;   // q - z, exact
-  return __builtin_bit_cast(uint32_t, d * sc);            // s * (q - z), rounded once
+  const f16x2 d = __builtin_bit_cast(f16x2, r) + zn[i];   // q - z, exact
+  return __builtin_bit_cast(uint32_t, d * sc);              // s * (q - z), rounded once
 }
 
-// {s, z} word -> packed (-(1024 + z), -(1024 + z)) and (s, s).
-__device__ __forceinline__ void sz_pair(uint32_t w, f16x2& zneg, f16x2& sc) {
+// {s, z} word -> zn[i] = packed -(M + z) for component i's magic M (exact:
+// integers <= 1279) and (s, s).
+template <int B>
+__device__ __forceinline__ void sz_pair(uint32_t w, f16x2 (&zn)[4], f16x2& sc) {
   const _Float16 s16 = __builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xFFFFu));
   const _Float16 z16 = __builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16));
-  const _Float16 zn = -(z16 + static_cast<_Float16>(1024.0f));   // exact: integer <= 1279
-  zneg = f16x2{zn, zn};
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const _Float16 v = -(z16 + static_cast<_Float16>(kMagicVal[kMagicOf<B>(i)]));
+    zn[i] = f16x2{v, v};
+  }
   sc = f16x2{s16, s16};
 }
 
@@ -348,9 +370,15 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
     for (int i = 0; i < NLD; i++) lds_dma16(xr, &st[64 * kTileWaves * i + 64 * wv], gv ? aoff[i] : kOOB, adv);
   };
 
-  // the OR operand of the unpacking in a vector register (one v_and_or_b32)
-  uint32_t vm = kMagic16;
-  asm volatile("" : "+v"(vm));
+  // the OR operands of the unpacking in vector registers (one v_and_or_b32
+  // each); only the magics the two widths use
+  uint32_t mg[4];
+#pragma unroll
+  for (int m = 0; m < 4; m++) {
+    mg[m] = kMagicAt[m];
+    const bool used = m == 0 || (m == 2 && (BW0 == 4 || BW1 == 4)) || BW0 == 2 || BW1 == 2;
+    if (used) asm volatile("" : "+v"(mg[m]));
+  }
   f32x16 acc0[TB], acc1[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; tb++) {
@@ -383,9 +411,9 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
       // eight K-step addresses are formed here, not kept live over the loop
       uint32_t a0 = static_cast<uint32_t>(n * SPT + ((kh * NM2) ^ (n % SPT)));
       asm volatile("" : "+v"(a0));
-      f16x2 zn0, sc0, zn1, sc1;
-      sz_pair(x0.szw, zn0, sc0);
-      sz_pair(x1.szw, zn1, sc1);
+      f16x2 zn0[4], sc0, zn1[4], sc1;
+      sz_pair<BW0>(x0.szw, zn0, sc0);
+      sz_pair<BW1>(x1.szw, zn1, sc1);
       // Software pipeline over the K-steps, fixed by scheduling fences (the
       // compiler would otherwise move each LDS read next to its first MFMA
       // and wait for it there): each MFMA of source 0 is issued with a
@@ -396,7 +424,7 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
 #pragma unroll
       for (int tb = 0; tb < TB; tb++) af[tb] = st[a0 + 32 * SPT * tb];
 #pragma unroll
-      for (int i = 0; i < 4; i++) b0[i] = dequant_h1<NM2, BW0>(x0.cw, 0, i, zn0, sc0, vm);
+      for (int i = 0; i < 4; i++) b0[i] = dequant_h1<NM2, BW0>(x0.cw, 0, i, zn0, sc0, mg);
 #pragma unroll
       for (int s = 0; s < NM2; s++) {
         const uint32_t an = a0 ^ static_cast<uint32_t>(s + 1);
@@ -404,7 +432,7 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
         for (int tb = 0; tb < TB; tb++) {
           acc0[tb] = mfma32h(af[tb], b0, acc0[tb]);
 #pragma unroll
-          for (int i = tb; i < 4; i += TB) b1[i] = dequant_h1<NM2, BW1>(x1.cw, s, i, zn1, sc1, vm);
+          for (int i = tb; i < 4; i += TB) b1[i] = dequant_h1<NM2, BW1>(x1.cw, s, i, zn1, sc1, mg);
           __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
@@ -413,7 +441,7 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
           if (s + 1 < NM2) {
             af[tb] = st[an + 32 * SPT * tb];
 #pragma unroll
-            for (int i = tb; i < 4; i += TB) b0[i] = dequant_h1<NM2, BW0>(x0.cw, s + 1, i, zn0, sc0, vm);
+            for (int i = tb; i < 4; i += TB) b0[i] = dequant_h1<NM2, BW0>(x0.cw, s + 1, i, zn0, sc0, mg);
           }
           __builtin_amdgcn_sched_barrier(0);
         }
