@@ -40,8 +40,8 @@ constexpr int kSharedSplitMax = 512;
 constexpr int kRoutedSplitMax = 48;
 constexpr int kTileWideFf = 4096;
 
-// Persistent tile grid: one workgroup of eight waves per compute unit (two
-// waves per SIMD), a multiple of the XCD count.
+// Persistent tile grid: kTileWgPerCu workgroups per compute unit (two waves
+// per SIMD in all), a multiple of the XCD count.
 int tile_grid() {
   static int cached[64] = {0};
   int dev = 0;
@@ -49,7 +49,7 @@ int tile_grid() {
   if (cached[dev] == 0) {
     int cu = 0;
     if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
-    cached[dev] = std::max(kXcds, cu / kXcds * kXcds);
+    cached[dev] = kTileWgPerCu * std::max(kXcds, cu / kXcds * kXcds);
   }
   return cached[dev];
 }

@@ -292,7 +292,12 @@ constexpr int kTileTok = 128;   // tokens per workgroup tile (four 32-token bloc
 template <int NK>
 constexpr int kTileWaveRows = NK == 2 ? 32 : 64;
 
-constexpr int kTileWaves = 8;
+// Workgroups of the tile kernel resident per compute unit, and its waves per
+// workgroup (two waves per SIMD in all) and LDS stages (three stages of one
+// workgroup or two of each of two fit the 160 KB of LDS).
+constexpr int kTileWgPerCu = 1;
+constexpr int kTileWaves = 8 / kTileWgPerCu;
+constexpr int kTileLdsStages = kTileWgPerCu == 1 ? 3 : 2;
 
 constexpr int kXcds = 8;
 constexpr int kSuper = 8;

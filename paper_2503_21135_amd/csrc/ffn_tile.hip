@@ -274,7 +274,8 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 // groups in flight) where the two sources' codes of a group take at most 16
 // registers, else 2 (the accumulators of both sources leave no room).
 template <int NM2, int BW0, int BW1>
-constexpr int kTileStages = ((kHalfWords<NM2, BW0>) + (kHalfWords<NM2, BW1>) <= 16) ? 3 : 2;
+constexpr int kTileStages =
+    (kTileLdsStages == 3 && (kHalfWords<NM2, BW0>) + (kHalfWords<NM2, BW1>) <= 16) ? 3 : 2;
 
 // Buffer source of one weight row of kind `kind`: the expert's own codes of
 // width be, or the cached 8-bit copy of the row (copy).
@@ -550,11 +551,11 @@ __device__ __forceinline__ void tile_dispatch(const FfnArgs& a, const TileLds& l
 // blocks, 128 registers) leave room for a second wave, which hides the
 // first one's load and LDS latencies.
 template <int NM2, int NK>
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(64 * kTileWaves) __attribute__((amdgpu_waves_per_eu(2)))
 ffn_tile_kernel(FfnArgs a, TileMap map, const int32_t* __restrict__ prefix) {
   __shared__ __attribute__((aligned(16))) u32x4 st0[TileStage<NM2>::SLOTS];
   __shared__ __attribute__((aligned(16))) u32x4 st1[TileStage<NM2>::SLOTS];
-  __shared__ __attribute__((aligned(16))) u32x4 st2[TileStage<NM2>::SLOTS];
+  __shared__ __attribute__((aligned(16))) u32x4 st2[kTileLdsStages == 3 ? TileStage<NM2>::SLOTS : 1];
   __shared__ int pre[MOE_MAX_EXPERTS + 1];
   const TileLds lds{st0, st1, st2};
   for (int i = threadIdx.x; i <= map.n_e; i += blockDim.x) pre[i] = prefix[i];
