@@ -21,8 +21,8 @@ namespace ffn {
 // exactly 1024 + q (q < 1024; 8-bit codes: one byte permute against bytes of
 // 0x64 per pair).  A code sitting higher in the word is OR-ed into a smaller
 // magic M whose mantissa unit falls on its lowest bit (64.0 for a 4-bit code
-// at bit 4; 256.0, 64.0, 16.0 for 2-bit codes at bits 2, 4, 6), which reads
-// M + q with no shift.  One packed fp16 subtraction of M + z makes q - z
+// at bit 4; 256.0, 64.0, 16.0 for 2-bit codes, and the low two bits of 3-bit
+// codes, at bits 2, 4, 6), which reads M + q with no shift.  One packed fp16 subtraction of M + z makes q - z
 // exactly, one packed fp16 multiplication by s rounds the product.
 //
 // Eight waves per workgroup, two per SIMD.  Each wave owns two weight rows
@@ -162,11 +162,12 @@ constexpr uint32_t kMagicAt[4] = {0x64006400u, 0x5C005C00u, 0x54005400u, 0x4C004
 constexpr float kMagicVal[4] = {1024.0f, 256.0f, 64.0f, 16.0f};
 
 // Magic of component i (weights 2i, 2i+1) of a K-step: 4-bit codes sit at
-// bits 0 and 4 of a byte (1024, 64), 2-bit codes at bits 0, 2, 4, 6 (1024,
-// 256, 64, 16); the other widths use 1024 throughout.
+// bits 0 and 4 of a byte (1024, 64), 2-bit codes and the low two bits of
+// 3-bit codes at bits 0, 2, 4, 6 (1024, 256, 64, 16; a 3-bit code's high bit
+// goes two bits above its low field); the other widths use 1024 throughout.
 template <int B>
 constexpr int kMagicOf(int i) {
-  return B == 2 ? i : (B == 4 ? 2 * (i & 1) : 0);
+  return (B == 2 || B == 3) ? i : (B == 4 ? 2 * (i & 1) : 0);
 }
 
 // Component i (weights 2i, 2i+1) of the B fragment of K-step s: two fp16
@@ -204,11 +205,16 @@ __device__ __forceinline__ uint32_t dequant_h1(const uint32_t (&cw)[(kHalfWords<
     const int o = (q & 1) * 8;
     r = (((lo >> (4 * i)) & 0x000F000Fu) | (((hi >> (o + 2 * i)) & 0x00030003u) << 4)) | mg[0];
   } else {  // 3-bit: per 32-code block words (low plane 0-15, low plane 16-31, high plane)
+    // pair pi = 4q + i: low bits at bits 2*(pi & 7) of its low-plane word
+    // (odd octets: the upper byte, shifted down once), high bit at bit pi of
+    // the high plane, moved to two bits above the low field
     const int blk = 3 * (s >> 2);
     const int q = s & 3;   // octet within the block
-    const uint32_t lo = cw[blk + (q >> 1)], hi = cw[blk + 2];
-    const int pi = 4 * q + i;   // pair index within the block
-    r = (((lo >> (2 * (pi & 7))) & 0x00030003u) | (((hi >> pi) & 0x00010001u) << 2)) | mg[0];
+    const uint32_t lo = (q & 1) ? cw[blk + (q >> 1)] >> 8 : cw[blk + (q >> 1)];
+    const uint32_t hi = cw[blk + 2];
+    const int sh = 4 * q + i - (2 * i + 2);   // high bit: from bit 4q + i to bit 2i + 2
+    const uint32_t hs = sh >= 0 ? hi >> sh : hi << -sh;
+    r = (lo & (0x00030003u << (2 * i))) | (hs & (0x00010001u << (2 * i + 2))) | mg[kMagicOf<3>(i)];
   }
   const f16x2 d = __builtin_bit_cast(f16x2, r) + zn[i];   // q - z, exact
   return __builtin_bit_cast(uint32_t, d * sc);              // s * (q - z), rounded once
@@ -377,7 +383,8 @@ __device__ __forceinline__ void tile_item(const FfnArgs& a, const TileLds& lds, 
 #pragma unroll
   for (int m = 0; m < 4; m++) {
     mg[m] = kMagicAt[m];
-    const bool used = m == 0 || (m == 2 && (BW0 == 4 || BW1 == 4)) || BW0 == 2 || BW1 == 2;
+    const bool used = m == 0 || (m == 2 && (BW0 == 4 || BW1 == 4)) || BW0 == 2 || BW1 == 2 || BW0 == 3 ||
+                      BW1 == 3;
     if (used) asm volatile("" : "+v"(mg[m]));
   }
   f32x16 acc0[TB], acc1[TB];
