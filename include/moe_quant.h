@@ -249,7 +249,9 @@ int moe_quant_pack(const float* w, int64_t ld_w, int32_t R, int32_t K,
  *             fmaf over c = l, l+64, l+128, ... in increasing c; then for
  *             off = 32, 16, 8, 4, 2, 1: partial[l] += partial[l+off] (l < off).
  *   topk_ids  device int32 [T][k]: the k experts of largest logit, ordered by
- *             (logit descending, expert index ascending).
+ *             (logit descending, expert index ascending); a NaN logit ranks as
+ *             -inf (in the softmax too), so the k ids are always distinct
+ *             experts in [0, E).
  *   topk_w    device fp32 [T][k]: softmax over the k selected logits,
  *             m = logit of slot 0, e_j = cexp(l_j - m), S = e_0 + e_1 + ...
  *             summed left to right, w_j = e_j / S.  cexp is the library's

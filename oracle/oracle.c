@@ -308,6 +308,9 @@ float oracle_cexp(float x) {
   return ldexpf(p, (int)n);
 }
 
+/* A logit as the top-k order sees it: NaN in the place of -inf. */
+static float rank_key(float v) { return isnan(v) ? -INFINITY : v; }
+
 /*
  * Router logits, top-k and combine weights.  The summation order of the
  * logit is fixed (the paper is silent; both implementations follow it so the
@@ -315,7 +318,9 @@ float oracle_cexp(float x) {
  * l accumulates fmaf over columns l, l+64, ... in increasing order, then a
  * halving tree partial[l] += partial[l+off], off = 32..1; then + bias.
  * Top-k by (logit descending, index ascending); weights are the softmax over
- * the k selected logits (weights sum to 1).
+ * the k selected logits (weights sum to 1).  The order is total over numbers
+ * only, so a NaN logit takes the place of -inf in the selection and in the
+ * softmax: the k picks are always k distinct experts.
  *
  *   x [T][d] bf16 patterns; Wr [E][d]; bias [E] or NULL;
  *   logits [T][E] (output, may be NULL); ids [T][k]; w [T][k].
@@ -349,15 +354,15 @@ int oracle_route(const uint16_t* x, int T, int d, const float* Wr,
         for (int i = 0; i < j; i++)
           if (id[i] == e) taken = 1;
         if (taken) continue;
-        if (best < 0 || lg[e] > lg[best]) best = e;
+        if (best < 0 || rank_key(lg[e]) > rank_key(lg[best])) best = e;
       }
       id[j] = best;
     }
     float ex[64];
-    float m = lg[id[0]];
+    float m = rank_key(lg[id[0]]);
     float S = 0.0f;
     for (int j = 0; j < k; j++) {
-      ex[j] = oracle_cexp(lg[id[j]] - m);
+      ex[j] = oracle_cexp(rank_key(lg[id[j]]) - m);
       S = S + ex[j];
     }
     for (int j = 0; j < k; j++) w[(int64_t)t * k + j] = ex[j] / S;

@@ -92,9 +92,10 @@ __device__ __forceinline__ void router_partials(const uint16_t* __restrict__ xr,
   }
 }
 
-// Top k of one token's E logits src[0 .. E) by (logit desc, index asc) and
-// the softmax over the selected logits; one wave, every lane ends with the
-// same picks, lane 0 writes the token's row of topk_ids / topk_w.
+// Top k of one token's E logits src[0 .. E) by (logit desc, index asc; a
+// NaN as -inf) and the softmax over the selected logits; one wave, every lane
+// ends with the same picks, lane 0 writes the token's row of topk_ids /
+// topk_w.
 __device__ __forceinline__ void select_topk(const float* src, int E, int k, int t, int lane,
                                             int32_t* __restrict__ topk_ids,
                                             float* __restrict__ topk_w) {
@@ -103,7 +104,8 @@ __device__ __forceinline__ void select_topk(const float* src, int E, int k, int 
 #pragma unroll
   for (int m = 0; m < kMaxPer; m++) {
     const int e = m * kWave + lane;
-    lg[m] = e < E ? src[e] : -INFINITY;
+    const float u = e < E ? src[e] : -INFINITY;
+    lg[m] = u != u ? -INFINITY : u;   // a NaN ranks as -inf
   }
   // top-k by (logit desc, index asc); every lane ends with the same picks
   bool taken[kMaxPer];
@@ -200,8 +202,9 @@ constexpr int kLogitTokens = 8;     // tokens of a logits workgroup
 constexpr int kSplitRouterMinT = 256;   // batches from this size: logits, then top k
 constexpr int kSplitRouterMinE = 16;    // smaller batches with this many experts too
 
-// Router logits of large batches with the experts spread over workgroups:
-// workgroup (token block, expert block) computes 8 tokens x 8 experts, wave w
+// Router logits of large batches whose rows are not 16-byte aligned, with the
+// experts spread over workgroups: workgroup (token block, expert block)
+// computes 8 tokens x 8 experts, wave w
 // experts 2w, 2w + 1 of the block, so a CU reads a slice of the router
 // matrix once for 8 tokens instead of the whole matrix per token.  Each
 // logit is the header's sum: lane l adds columns l, l + 64, ... in ascending

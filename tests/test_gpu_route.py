@@ -92,6 +92,22 @@ def test_route_misaligned_rows(orc, T):
     assert np.array_equal(g["w"].view(np.uint32), w.view(np.uint32))
 
 
+@pytest.mark.parametrize("T,E,k,n_nan", [(20, 8, 2, 1), (20, 8, 4, 6), (300, 8, 4, 6), (40, 20, 4, 18),
+                                         (300, 20, 3, 2)])
+def test_route_nan_logits_rank_as_minus_inf(orc, T, E, k, n_nan):
+    # experts whose router rows are NaN have NaN logits for every token; they
+    # rank as -inf on every router form (one workgroup per token, staged
+    # logits with the rank selection), so the ids stay valid experts and match
+    # the oracle, and a NaN pick gets weight 0
+    rng = np.random.default_rng(T + E + n_nan)
+    d = 256
+    x = mi.bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    router = (rng.standard_normal((E, d)) * 0.02).astype(np.float32)
+    router[:n_nan] = np.nan
+    g = check_route(orc, x, router, None, k, 1)
+    assert np.all((g["ids"] >= 0) & (g["ids"] < E))
+
+
 def test_route_ties_and_empty_experts(orc):
     rng = np.random.default_rng(3)
     d, E = 256, 16

@@ -6,6 +6,8 @@ Router (Sec. II-A: a fixed number k of experts per token):
   R3  top-k equals a full lexicographic sort (logit desc, index asc)
   R4  weights are the softmax over the selected logits (fp64 reference),
       non-negative, summing to 1 within 2k ulp; ties go to the lower index
+  R5  a NaN logit ranks as -inf: never picked while k numbers are left, and
+      the picks are always k distinct experts
 Permutation (one-to-many token -> expert mapping as per-expert segments):
   P1  segments partition the T*k assignments, offsets are the expert counts,
       tokens ascend within a segment, inv_perm inverts perm_token, and the
@@ -90,6 +92,27 @@ def test_r4_ties_go_to_lower_index(orc):
         assert lg[t, 4] == lg[t, 6] and lg[t, 5] == lg[t, 7]
         if 4 in ids[t] and 6 in ids[t]:
             assert list(ids[t]).index(4) < list(ids[t]).index(6)
+
+
+@pytest.mark.parametrize("nan_rows,k", [((3,), 2), ((0, 1, 2, 3, 4, 5), 4)])
+def test_r5_nan_logits_rank_as_minus_inf(orc, nan_rows, k):
+    x, Wr, _ = _route_case(T=16, E=8, k=k, seed=9)
+    Wr[list(nan_rows)] = np.nan           # those experts' logits are NaN for every token
+    lg, ids, w = orc.route(x, Wr, k)
+    finite = [e for e in range(8) if e not in nan_rows]
+    for t in range(16):
+        assert np.all(np.isnan(lg[t, list(nan_rows)]))
+        key = lambda e: (math.inf, e) if e in nan_rows else (-float(lg[t, e]), e)   # NaN after every number
+        assert list(ids[t]) == sorted(range(8), key=key)[:k]
+        assert len(set(ids[t])) == k and all(0 <= e < 8 for e in ids[t])
+        # the picked NaN experts enter the softmax as -inf: weight 0, and the
+        # finite picks' weights are the softmax over the finite logits alone
+        picked = [e for e in ids[t] if e in finite]
+        ref = np.exp(np.float64(lg[t, picked]) - np.float64(lg[t, picked]).max())
+        ref /= ref.sum()
+        got = np.array([w[t, j] for j in range(k) if ids[t, j] in finite], np.float64)
+        assert np.allclose(got, ref, rtol=2e-6)
+        assert all(w[t, j] == 0.0 for j in range(k) if ids[t, j] in nan_rows)
 
 
 @pytest.mark.parametrize("T,E,k,S", [(64, 8, 2, 0), (50, 64, 6, 2), (33, 60, 4, 1),
