@@ -294,13 +294,13 @@ __device__ __forceinline__ void tree_scatter(float (&a)[NV], int lane) {
 
 // Router logits staged through LDS: workgroup (token block of 4*WT tokens,
 // expert block of WE experts) copies SC-column chunks of its token rows
-// (bf16) and router rows (fp32) into LDS with 16-byte loads,
-// the next chunk's loads in flight while the current one is used; wave w
-// holds the WT x WE logits of tokens 4w.. of the block, lane l adding columns
-// l, l + 64, ... in ascending order with one FMA each (the header's per-lane
-// order), then the halving tree over the lanes (tree_scatter) and the bias.
-// x and wr must be 16-byte aligned; tokens and experts past the ends are
-// clamped (computed, not stored).
+// (bf16) and router rows (fp32) into LDS with 16-byte loads, the next
+// chunk's loads in flight while the current one is used.  Wave w holds the
+// logits of tokens WT*w .. WT*w + WT - 1 of the block against the WE experts,
+// lane l adding columns l, l + 64, ... in ascending order with one FMA each
+// (the header's per-lane order), then the halving tree over the lanes
+// (tree_scatter) and the bias.  x and wr must be 16-byte aligned; tokens and
+// experts past the ends are clamped (computed, not stored).
 template <int WT, int WE, int SC>
 __global__ void __launch_bounds__(4 * kWave)
 route_logits_lds_kernel(const uint16_t* __restrict__ x, int T, int d, const float* __restrict__ wr,
