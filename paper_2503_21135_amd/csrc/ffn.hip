@@ -228,10 +228,10 @@ int64_t stream_grid(const WgMap& m) {
   return static_cast<int64_t>(m.n_r) * m.n_sw * m.m_r + (m.n_ent > 0 ? m.ent_start[m.n_ent] : 0);
 }
 
-TileMap tile_map(const moe_layer_t* L, bool shared, int n_split) {
+TileMap tile_map(const moe_layer_t* L, int e0, int n_e, int n_split) {
   TileMap m{};
-  m.e0 = shared ? L->n_experts : 0;
-  m.n_e = shared ? L->n_shared : L->n_experts;
+  m.e0 = e0;
+  m.n_e = n_e;
   m.n_split = n_split;
   for (int i = 0; i < m.n_e; i++) m.bits[i] = static_cast<int8_t>(L->bits_host[m.e0 + i]);
   return m;
@@ -294,10 +294,15 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     if (S > 0) prep(a.Tk, a.rows, p.nt_shared == 0);
   }
   int32_t* prefix = a.tile_prefix;
-  // tile path: plan kernel, then the persistent tile kernel, for one expert set
-  auto add_tile = [&](std::vector<Launch>& v, auto nk, bool shared) {
+  // tile path: plan kernel, then the persistent tile kernel, over the experts
+  // that take it -- routed, shared, or both in one launch (routed first), so
+  // that one persistent grid balances all of their items
+  const bool tile_r = p.nt_routed == 0, tile_s = S > 0 && p.nt_shared == 0;
+  auto add_tile = [&](std::vector<Launch>& v, auto nk) {
     constexpr int NK = decltype(nk)::value;
-    const TileMap m = tile_map(L, shared, NK == 1 ? p.n_split : 1);
+    if (!tile_r && !tile_s) return;
+    const int e0 = tile_r ? 0 : a.E, n_e = (tile_r ? a.E : 0) + (tile_s ? S : 0);
+    const TileMap m = tile_map(L, e0, n_e, NK == 1 ? p.n_split : 1);
     const int32_t* pf = prefix;
     prefix += MOE_MAX_EXPERTS + 1;
     if (m.n_e == 0) return;
@@ -327,8 +332,7 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
   };
   using two = std::integral_constant<int, 2>;
   using one = std::integral_constant<int, 1>;
-  if (p.nt_routed == 0) add_tile(gate_up, two{}, false);
-  if (S > 0 && p.nt_shared == 0) add_tile(gate_up, two{}, true);
+  add_tile(gate_up, two{});
   add_stream(gate_up, two{}, 1);
   {  // group sums of h, [max(f,fs)/g][rows], for the rows the streaming kernel reads
     // (routed rows f wide, shared rows fs wide; one launch when both stream)
@@ -345,8 +349,7 @@ void launch_all(const FfnArgs& a, const Plan& p, const moe_layer_t* L, int T, hi
     else if (rs) hs(0, a.Tk);
     else if (ss) hs(a.Tk, a.rows);
   }
-  if (p.nt_routed == 0) add_tile(down, one{}, false);
-  if (S > 0 && p.nt_shared == 0) add_tile(down, one{}, true);
+  add_tile(down, one{});
   add_stream(down, one{}, p.n_split);
   issue(xsum, event(0), nullptr, s);
   issue(gate_up, event(1), event(2), s);
