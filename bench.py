@@ -1055,8 +1055,9 @@ def main():
     # peak against its algorithmic flops at the bf16 MFMA peak.
     hbm_bound = byt["gate_up"] / HBM_PEAK_GBS >= flops_gate_up(layer, offsets) / 1e3 / BF16_PEAK_TFLOPS
     kernel = ("FFN gate/up stage (gate+up projections, SiLU-GLU epilogue): ffn_stream_kernel "
-              "for up to 28 tokens per expert, else tile_plan_kernel + ffn_tile_kernel; "
-              "routed experts, then shared experts where the layer has them")
+              "for up to 28 tokens per expert (48 for experts narrower than d_ff 4096; shared "
+              "experts up to 512 tokens), else tile_plan_kernel + ffn_tile_kernel; routed and "
+              "shared experts in one launch per kernel")
     if hbm_bound:
         roof = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved_gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
